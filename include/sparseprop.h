@@ -1,0 +1,234 @@
+/*
+ * sparseprop.h -- C ABI of libsparseprop.so, an MI355X (gfx950) implementation
+ * of the sparse forward/backward passes of SparseProp (Nikdan et al., "SparseProp:
+ * Efficient Sparse Backpropagation for Faster Training of Neural Networks",
+ * ICML 2023).
+ *
+ * General conventions
+ * -------------------
+ *  - Every pointer argument is a DEVICE pointer unless its description says
+ *    "host".  All buffers are allocated and owned by the caller; the library
+ *    never allocates, frees or keeps a pointer after a call returns.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *    device operation is enqueued asynchronously on it; no call synchronises
+ *    the host.  Callers must keep inputs alive and unmodified until the
+ *    stream has passed the call.
+ *  - Outputs are overwritten, never accumulated: Y and dX include exact zeros
+ *    where no stored weight contributes, and dW holds exactly one value per
+ *    stored weight.  Inputs are never modified.
+ *  - Values are fp32 and the arithmetic is fp32 fused multiply-add; results
+ *    match the exact sum to within ~1e-6 of the sum of absolute terms.
+ *    Integer/structure outputs are exact and deterministic.  All ops are
+ *    deterministic: the same inputs give bitwise identical outputs.
+ *  - Errors: cheap argument checks run on the host before anything is
+ *    enqueued and return a status (nothing is launched on error).  Launch
+ *    failures return SP_ERR_HIP.  Structural validity of index arrays
+ *    (monotone pointers, indices in range, sorted columns) is a precondition
+ *    of the compute ops; sp_*_validate checks it on the host for debugging.
+ *  - Sizes are int64_t; nnz must be < 2^31.  The ops are thread-safe: the
+ *    library holds no mutable global state.
+ *
+ * Layouts
+ * -------
+ *  Linear: W is stored as out_f x in_f (PyTorch's layout; it is the transpose
+ *  of the M x N matrix W of the paper's Sec. 3.2, with M = in_f and N = out_f)
+ *  in CSR form (Sec. 3.2, "Sparse Representation"): the stored entries of row
+ *  i are [row_ptr[i], row_ptr[i+1]), with input-column indices col_idx[]
+ *  strictly ascending within a row and values vals[].  X and dX are [B][in_f],
+ *  Y and dY are [B][out_f]; all dense tensors are row-major and contiguous.
+ *
+ *  Convolution: NCHW.  X, dX are [B][IC][H][W]; Y, dY are [B][OC][OH][OW];
+ *  the weight is [OC][IC][KH][KW] stored in the paper's five-array format
+ *  (Sec. 3.3, "Sparse Representation"):
+ *     w_oc[OC+1]       int32  start of each output channel's entries
+ *     w_ic[OC*(IC+1)]  int16  offsets of each input channel inside an output
+ *                             channel: entries of (oc, ic) are
+ *                             [w_oc[oc] + w_ic[oc*(IC+1)+ic],
+ *                              w_oc[oc] + w_ic[oc*(IC+1)+ic+1])
+ *     w_x[nnz], w_y[nnz] uint8 kernel row (dim 2) and column (dim 3)
+ *     w_vals[nnz]      fp32   values
+ *  Entries of one (oc, ic) are in (x, y) row-major order.  Convolution is
+ *  cross-correlation with symmetric zero padding, dilation 1, groups 1 and no
+ *  bias: OH = floor((H + 2*pad_h - KH)/stride_h) + 1 (likewise OW).  The paper
+ *  derives Eq. 3-5 at stride 1 / pad 0; the padded bounds follow its
+ *  Algorithm 2, and stride follows the same sampling.
+ */
+#ifndef SPARSEPROP_H
+#define SPARSEPROP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int sp_status;
+#define SP_OK 0
+#define SP_ERR_INVALID_ARG 1  /* null pointer with nonzero size, negative or inconsistent size */
+#define SP_ERR_UNSUPPORTED 2  /* valid but outside the supported range (e.g. KH > 255) */
+#define SP_ERR_HIP 3          /* a HIP runtime call or kernel launch failed */
+#define SP_ERR_WORKSPACE 4    /* workspace missing or smaller than the *_ws query says */
+
+/* Host.  Static, never-freed description of a status code. */
+const char *sp_status_string(sp_status s);
+
+/* Host.  Library version string. */
+const char *sp_version(void);
+
+/* ======================================================================== */
+/* Linear layers (Sec. 3.2)                                                 */
+/* ======================================================================== */
+
+/* Structure preparation, step 1 of 2: CSR row pointers of a dense pattern.
+ * mask: uint8 [out_f][in_f], nonzero = stored entry (the pattern, not the
+ * values, defines the structure; a stored weight may be 0.0).
+ * row_ptr: out [out_f+1].  The caller reads row_ptr[out_f] (= nnz) back to
+ * size col_idx/vals.  Requires nnz < 2^31. */
+sp_status sp_linear_encode_rows(int64_t out_f, int64_t in_f, const uint8_t *mask,
+                                int32_t *row_ptr, void *stream);
+
+/* Structure preparation, step 2 of 2: column indices (ascending within a
+ * row) and values of the stored entries.  W: fp32 [out_f][in_f] dense
+ * values; row_ptr from step 1; col_idx, vals: out [nnz]. */
+sp_status sp_linear_encode_fill(int64_t out_f, int64_t in_f, const uint8_t *mask,
+                                const float *W, const int32_t *row_ptr,
+                                int32_t *col_idx, float *vals, void *stream);
+
+/* CSC view of the CSR pattern (the paper's remark that the transpose of a
+ * CSR matrix is the same matrix in CSC form, Sec. 3.2 "Implementation
+ * Details").  For input column r, entries [t_col_ptr[r], t_col_ptr[r+1]) list
+ * the output rows t_row_idx[] in ascending order, and t_perm[] holds the CSR
+ * position of each entry.  Outputs: t_col_ptr [in_f+1], t_row_idx [nnz],
+ * t_perm [nnz].  Built once per mask; bit-exact and deterministic. */
+sp_status sp_linear_transpose(int64_t in_f, int64_t out_f, const int32_t *row_ptr,
+                              const int32_t *col_idx, int64_t nnz,
+                              int32_t *t_col_ptr, int32_t *t_row_idx,
+                              int32_t *t_perm, void *stream);
+
+/* Forward pass (Sec. 3.2: O = X W, here Y = X W^T with W out_f x in_f):
+ *   Y[t,i] = sum_{j in row i} vals[j] * X[t, col_idx[j]].
+ * X: [B][in_f]; Y: out [B][out_f]. */
+sp_status sp_linear_fwd(const float *X, int64_t B, int64_t in_f, int64_t out_f,
+                        const int32_t *row_ptr, const int32_t *col_idx,
+                        const float *vals, int64_t nnz, float *Y, void *stream);
+
+/* Workspace bytes needed by sp_linear_bwd_input (host). */
+sp_status sp_linear_bwd_input_ws(int64_t B, int64_t in_f, int64_t out_f,
+                                 int64_t nnz, size_t *bytes);
+
+/* Input gradient, Eq. 1 (dL/dX = dL/dO W^T in the paper's notation; here
+ * dX = dY W with W out_f x in_f):
+ *   dX[t,r] = sum_{(i,r) stored} vals[(i,r)] * dY[t,i].
+ * Computed per input column r over the CSC view, so each dX element has one
+ * writer and no atomics are used.  dY: [B][out_f]; t_* from
+ * sp_linear_transpose; vals in CSR order; dX: out [B][in_f].
+ * workspace: device scratch of sp_linear_bwd_input_ws() bytes. */
+sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f,
+                              const int32_t *t_col_ptr, const int32_t *t_row_idx,
+                              const int32_t *t_perm, const float *vals, int64_t nnz,
+                              float *dX, void *workspace, size_t ws_bytes,
+                              void *stream);
+
+/* Workspace bytes needed by sp_linear_bwd_weight (host). */
+sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f,
+                                  int64_t nnz, size_t *bytes);
+
+/* Weight gradient, Eq. 2 sampled at the stored entries (an SDDMM with nnz
+ * dot products of length B):
+ *   dW[j] = sum_t dY[t, row(j)] * X[t, col_idx[j]]   for every stored j,
+ * in CSR order.  The reduction over t is split across workgroups and summed
+ * in a fixed order in a second pass (deterministic).  dW: out [nnz]. */
+sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64_t B,
+                               int64_t in_f, int64_t out_f, const int32_t *row_ptr,
+                               const int32_t *col_idx, int64_t nnz, float *dW,
+                               void *workspace, size_t ws_bytes, void *stream);
+
+/* Host.  Structural check of a CSR pattern held in HOST memory: returns
+ * SP_OK or SP_ERR_INVALID_ARG (row_ptr not monotone, row_ptr[0] != 0,
+ * row_ptr[out_f] != nnz, column out of range or not strictly ascending). */
+sp_status sp_linear_validate(int64_t in_f, int64_t out_f, const int32_t *row_ptr,
+                             const int32_t *col_idx, int64_t nnz);
+
+/* ======================================================================== */
+/* Convolutions (Sec. 3.3)                                                  */
+/* ======================================================================== */
+
+typedef struct {
+    int64_t B, IC, H, W, OC;
+    int32_t KH, KW, stride_h, stride_w, pad_h, pad_w;
+} sp_conv_shape;
+
+/* Host.  Output spatial size; SP_ERR_INVALID_ARG if the shape is invalid
+ * (non-positive sizes, stride < 1, pad < 0, or an empty output). */
+sp_status sp_conv_out_hw(const sp_conv_shape *s, int64_t *OH, int64_t *OW);
+
+/* Structure preparation, step 1 of 2: w_oc [OC+1] and w_ic [OC*(IC+1)] of a
+ * dense pattern mask [OC][IC][KH][KW] (uint8, nonzero = stored).  Requires
+ * KH, KW <= 255 and IC*KH*KW <= 32767 (so every per-channel offset fits in
+ * int16), else SP_ERR_UNSUPPORTED.  The caller reads w_oc[OC] (= nnz). */
+sp_status sp_conv_encode_rows(int64_t OC, int64_t IC, int32_t KH, int32_t KW,
+                              const uint8_t *mask, int32_t *w_oc, int16_t *w_ic,
+                              void *stream);
+
+/* Structure preparation, step 2 of 2: w_x, w_y, w_vals [nnz] from the dense
+ * pattern and fp32 values W [OC][IC][KH][KW]. */
+sp_status sp_conv_encode_fill(int64_t OC, int64_t IC, int32_t KH, int32_t KW,
+                              const uint8_t *mask, const float *W,
+                              const int32_t *w_oc, const int16_t *w_ic,
+                              uint8_t *w_x, uint8_t *w_y, float *w_vals,
+                              void *stream);
+
+/* Input-channel-major view of the format (Algorithm 2 traverses input
+ * channels outermost).  For input channel ic, entries
+ * [t_ic_ptr[ic], t_ic_ptr[ic+1]) list the stored entries with that input
+ * channel in ascending (oc, x, y) order; t_oc holds the output channel and
+ * t_perm the index into w_x/w_y/w_vals.  Outputs: t_ic_ptr [IC+1],
+ * t_oc [nnz], t_perm [nnz].  Built once per mask; bit-exact. */
+sp_status sp_conv_transpose(int64_t OC, int64_t IC, const int32_t *w_oc,
+                            const int16_t *w_ic, int64_t nnz, int32_t *t_ic_ptr,
+                            int32_t *t_oc, int32_t *t_perm, void *stream);
+
+/* Forward pass, Eq. 3 with stride and padding:
+ *   Y[b,oc,p,q] = sum over entries si of oc of
+ *                 w_vals[si] * X[b, ic(si), p*sh + w_x[si] - ph, q*sw + w_y[si] - pw]
+ * (taps in the zero padding contribute nothing).  Y: out [B][OC][OH][OW]. */
+sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const int32_t *w_oc,
+                      const int16_t *w_ic, const uint8_t *w_x, const uint8_t *w_y,
+                      const float *w_vals, int64_t nnz, float *Y, void *stream);
+
+/* Workspace bytes needed by sp_conv_bwd_input (host). */
+sp_status sp_conv_bwd_input_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
+
+/* Input gradient, Eq. 4 with stride and padding: every term of Eq. 3 that
+ * reads X[b,ic,m,n] contributes w_vals[si] * dY[b,oc,p,q] to dX[b,ic,m,n].
+ * Computed per input channel over the ic-major view (one writer per dX
+ * element, no atomics).  t_* from sp_conv_transpose.  dX: out [B][IC][H][W]. */
+sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s,
+                            const uint8_t *w_x, const uint8_t *w_y,
+                            const float *w_vals, const int32_t *t_ic_ptr,
+                            const int32_t *t_oc, const int32_t *t_perm, int64_t nnz,
+                            float *dX, void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by sp_conv_bwd_weight (host). */
+sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
+
+/* Weight gradient, Eq. 5 with stride and padding, only for stored entries:
+ *   dW[si] = sum_{b,p,q} dY[b,oc,p,q] * X[b, ic, p*sh + x - ph, q*sw + y - pw]
+ * in the format's entry order.  Deterministic split reduction over
+ * (b, p, q).  dW: out [nnz]. */
+sp_status sp_conv_bwd_weight(const float *dY, const float *X, const sp_conv_shape *s,
+                             const int32_t *w_oc, const int16_t *w_ic,
+                             const uint8_t *w_x, const uint8_t *w_y, int64_t nnz,
+                             float *dW, void *workspace, size_t ws_bytes, void *stream);
+
+/* Host.  Structural check of a five-array pattern held in HOST memory. */
+sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW,
+                           const int32_t *w_oc, const int16_t *w_ic,
+                           const uint8_t *w_x, const uint8_t *w_y, int64_t nnz);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SPARSEPROP_H */
