@@ -100,35 +100,55 @@ sp_status sp_linear_encode_fill(int64_t out_f, int64_t in_f, const uint8_t *mask
  * Details").  For input column r, entries [t_col_ptr[r], t_col_ptr[r+1]) list
  * the output rows t_row_idx[] in ascending order, and t_perm[] holds the CSR
  * position of each entry.  Outputs: t_col_ptr [in_f+1], t_row_idx [nnz],
- * t_perm [nnz].  Built once per mask; bit-exact and deterministic. */
+ * t_perm [nnz].  scratch: device buffer of sp_linear_transpose_ws() bytes.
+ * Bit-exact and deterministic. */
+sp_status sp_linear_transpose_ws(int64_t in_f, int64_t out_f, int64_t nnz,
+                                 size_t *bytes);
 sp_status sp_linear_transpose(int64_t in_f, int64_t out_f, const int32_t *row_ptr,
                               const int32_t *col_idx, int64_t nnz,
                               int32_t *t_col_ptr, int32_t *t_row_idx,
-                              int32_t *t_perm, void *stream);
+                              int32_t *t_perm, void *scratch, size_t scratch_bytes,
+                              void *stream);
+
+/* Plan: the mask's structure prepared once (the paper notes that masks
+ * change only a few times per training run).  A plan is an opaque device
+ * buffer of sp_linear_plan_bytes() bytes, built from the CSR pattern by
+ * sp_linear_plan() on the device.  It holds the CSC view and, for both
+ * orientations of W, the stored entries regrouped into tiles of 128 rows x
+ * 64 columns with per-row segment offsets, so that the compute kernels stage
+ * one dense 64-column slab in LDS and visit exactly the entries that read
+ * it.  The plan depends on the pattern only, never on the values: vals may
+ * change freely between calls (in CSR order).  The caller keeps the plan
+ * alive while ops that use it are in flight.  It stays valid for any B. */
+sp_status sp_linear_plan_bytes(int64_t in_f, int64_t out_f, int64_t nnz,
+                               size_t *bytes);
+sp_status sp_linear_plan(int64_t in_f, int64_t out_f, const int32_t *row_ptr,
+                         const int32_t *col_idx, int64_t nnz, void *plan,
+                         size_t plan_bytes, void *stream);
+
+/* Copy the CSC view held in a plan into caller buffers (t_col_ptr [in_f+1],
+ * t_row_idx [nnz], t_perm [nnz]); same content as sp_linear_transpose. */
+sp_status sp_linear_plan_csc(const void *plan, int64_t in_f, int64_t out_f,
+                             int64_t nnz, int32_t *t_col_ptr, int32_t *t_row_idx,
+                             int32_t *t_perm, void *stream);
 
 /* Forward pass (Sec. 3.2: O = X W, here Y = X W^T with W out_f x in_f):
  *   Y[t,i] = sum_{j in row i} vals[j] * X[t, col_idx[j]].
- * X: [B][in_f]; Y: out [B][out_f]. */
+ * X: [B][in_f]; vals: [nnz] in CSR order; plan from sp_linear_plan;
+ * Y: out [B][out_f]. */
 sp_status sp_linear_fwd(const float *X, int64_t B, int64_t in_f, int64_t out_f,
-                        const int32_t *row_ptr, const int32_t *col_idx,
-                        const float *vals, int64_t nnz, float *Y, void *stream);
-
-/* Workspace bytes needed by sp_linear_bwd_input (host). */
-sp_status sp_linear_bwd_input_ws(int64_t B, int64_t in_f, int64_t out_f,
-                                 int64_t nnz, size_t *bytes);
+                        const float *vals, int64_t nnz, const void *plan,
+                        float *Y, void *stream);
 
 /* Input gradient, Eq. 1 (dL/dX = dL/dO W^T in the paper's notation; here
  * dX = dY W with W out_f x in_f):
  *   dX[t,r] = sum_{(i,r) stored} vals[(i,r)] * dY[t,i].
- * Computed per input column r over the CSC view, so each dX element has one
- * writer and no atomics are used.  dY: [B][out_f]; t_* from
- * sp_linear_transpose; vals in CSR order; dX: out [B][in_f].
- * workspace: device scratch of sp_linear_bwd_input_ws() bytes. */
-sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f,
-                              const int32_t *t_col_ptr, const int32_t *t_row_idx,
-                              const int32_t *t_perm, const float *vals, int64_t nnz,
-                              float *dX, void *workspace, size_t ws_bytes,
-                              void *stream);
+ * Computed per input column r over the plan's CSC tiles, so each dX element
+ * has one writer and no atomics are used.  dY: [B][out_f]; vals in CSR
+ * order; dX: out [B][in_f]. */
+sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f,
+                              int64_t out_f, const float *vals, int64_t nnz,
+                              const void *plan, float *dX, void *stream);
 
 /* Workspace bytes needed by sp_linear_bwd_weight (host). */
 sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f,
@@ -137,12 +157,14 @@ sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f,
 /* Weight gradient, Eq. 2 sampled at the stored entries (an SDDMM with nnz
  * dot products of length B):
  *   dW[j] = sum_t dY[t, row(j)] * X[t, col_idx[j]]   for every stored j,
- * in CSR order.  The reduction over t is split across workgroups and summed
- * in a fixed order in a second pass (deterministic).  dW: out [nnz]. */
+ * written in CSR order.  The reduction over t is split across workgroups
+ * into the workspace and summed in a fixed order by a second kernel
+ * (deterministic).  dW: out [nnz]; workspace: sp_linear_bwd_weight_ws()
+ * bytes. */
 sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64_t B,
-                               int64_t in_f, int64_t out_f, const int32_t *row_ptr,
-                               const int32_t *col_idx, int64_t nnz, float *dW,
-                               void *workspace, size_t ws_bytes, void *stream);
+                               int64_t in_f, int64_t out_f, int64_t nnz,
+                               const void *plan, float *dW, void *workspace,
+                               size_t ws_bytes, void *stream);
 
 /* Host.  Structural check of a CSR pattern held in HOST memory: returns
  * SP_OK or SP_ERR_INVALID_ARG (row_ptr not monotone, row_ptr[0] != 0,

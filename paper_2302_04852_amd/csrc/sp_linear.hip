@@ -1,0 +1,517 @@
+// Sparse linear layers on gfx950 (SparseProp Sec. 3.2): structure
+// preparation -- encoders from a dense pattern, the CSC view and the tiled
+// plan -- and the three passes: forward product, input gradient (Eq. 1) and
+// weight gradient sampled at the stored entries (Eq. 2).  The compute work
+// runs in the tiled kernels of sp_tiled.h; this file supplies the linear
+// geometry: tokens are rows of row-major [B][features] matrices.
+#include "sp_tiled.h"
+
+namespace {
+
+using spt::C;
+using spt::NTHR;
+using spt::NW;
+using spt::PF;
+using spt::T;
+using spt::TS;
+
+constexpr int TR_BLK = 32;  // rows per block of the stable transpose
+
+// --------------------------------------------------------------------------
+// Encoders: dense pattern -> CSR.  One wave per row; lanes scan 64 columns at
+// a time and compact with a ballot.
+
+__global__ __launch_bounds__(256) void k_encode_rows(const uint8_t *__restrict__ mask, int64_t out_f,
+                                                     int64_t in_f, int32_t *__restrict__ row_ptr) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= out_f) return;
+    const uint8_t *m = mask + row * in_f;
+    int cnt = 0;
+    for (int64_t c = lane; c < in_f; c += 64) cnt += (m[c] != 0);
+    for (int d = 32; d >= 1; d >>= 1) cnt += __shfl_xor(cnt, d, 64);
+    if (lane == 0) row_ptr[row + 1] = cnt;
+}
+
+__global__ __launch_bounds__(256) void k_encode_fill(const uint8_t *__restrict__ mask,
+                                                     const float *__restrict__ W, int64_t out_f,
+                                                     int64_t in_f, const int32_t *__restrict__ row_ptr,
+                                                     int32_t *__restrict__ col_idx,
+                                                     float *__restrict__ vals) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= out_f) return;
+    int32_t pos = row_ptr[row];
+    for (int64_t c0 = 0; c0 < in_f; c0 += 64) {
+        const int64_t c = c0 + lane;
+        const bool on = (c < in_f) && mask[row * in_f + c] != 0;
+        const uint64_t bal = __ballot(on);
+        if (on) {
+            const int before = __popcll(bal & ((1ull << lane) - 1ull));
+            col_idx[pos + before] = (int32_t)c;
+            vals[pos + before] = W[row * in_f + c];
+        }
+        pos += __popcll(bal);
+    }
+}
+
+// --------------------------------------------------------------------------
+// Stable CSR -> CSC.  Rows are cut into blocks of TR_BLK; blk_cnt[b][c] counts
+// the entries of column c in block b.  A per-column exclusive scan over the
+// blocks turns these into starting offsets, and one wave per block then
+// walks its rows in order with per-column counters held in LDS, so every
+// column lists its rows in ascending order.
+
+__global__ __launch_bounds__(256) void k_csc_count(const int32_t *__restrict__ row_ptr,
+                                                   const int32_t *__restrict__ col_idx, int64_t out_f,
+                                                   int64_t in_f, int32_t *__restrict__ blk_cnt,
+                                                   int32_t *__restrict__ col_cnt) {
+    const int lane = threadIdx.x & 63;
+    const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (row >= out_f) return;
+    const int64_t b = row / TR_BLK;
+    for (int32_t j = row_ptr[row] + lane; j < row_ptr[row + 1]; j += 64) {
+        const int32_t c = col_idx[j];
+        atomicAdd(&blk_cnt[b * in_f + c], 1);
+        atomicAdd(&col_cnt[c + 1], 1);
+    }
+}
+
+// Per column: exclusive scan over blocks (in place), offset by t_col_ptr.
+__global__ __launch_bounds__(256) void k_csc_block_offsets(int32_t *__restrict__ blk_cnt, int64_t nblk,
+                                                           int64_t in_f,
+                                                           const int32_t *__restrict__ t_col_ptr) {
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= in_f) return;
+    int32_t run = t_col_ptr[c];
+    for (int64_t b = 0; b < nblk; ++b) {
+        const int32_t v = blk_cnt[b * in_f + c];
+        blk_cnt[b * in_f + c] = run;
+        run += v;
+    }
+}
+
+// One wave per block.  ctr[] (dynamic LDS, in_f ints) holds the next free
+// slot of each column for this block.
+__global__ __launch_bounds__(64) void k_csc_fill(const int32_t *__restrict__ row_ptr,
+                                                 const int32_t *__restrict__ col_idx, int64_t out_f,
+                                                 int64_t in_f, const int32_t *__restrict__ blk_off,
+                                                 int32_t *__restrict__ t_row_idx,
+                                                 int32_t *__restrict__ t_perm) {
+    extern __shared__ int32_t ctr[];
+    const int lane = threadIdx.x;
+    const int64_t b = blockIdx.x;
+    for (int64_t c = lane; c < in_f; c += 64) ctr[c] = blk_off[b * in_f + c];
+    __syncthreads();
+    const int64_t r0 = b * TR_BLK;
+    const int64_t r1 = (r0 + TR_BLK < out_f) ? r0 + TR_BLK : out_f;
+    for (int64_t row = r0; row < r1; ++row) {
+        for (int32_t j = row_ptr[row] + lane; j < row_ptr[row + 1]; j += 64) {
+            const int32_t c = col_idx[j];
+            const int32_t pos = ctr[c];
+            ctr[c] = pos + 1;  // columns are distinct within a row
+            t_row_idx[pos] = (int32_t)row;
+            t_perm[pos] = j;
+        }
+        __syncthreads();  // order the counter updates of consecutive rows
+    }
+}
+
+sp_status csc_build(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
+                    int64_t nnz, int32_t *t_col_ptr, int32_t *t_row_idx, int32_t *t_perm,
+                    int32_t *blk_cnt, hipStream_t st) {
+    const int64_t nblk = sp::ceil_div(out_f, TR_BLK);
+    sp_status s;
+    if ((s = sp::fill_i32(t_col_ptr, in_f + 1, 0, st))) return s;
+    if ((s = sp::fill_i32(blk_cnt, nblk * in_f, 0, st))) return s;
+    if (out_f > 0 && nnz > 0) {
+        hipLaunchKernelGGL(k_csc_count, dim3((unsigned)sp::ceil_div(out_f, 4)), dim3(256), 0, st,
+                           row_ptr, col_idx, out_f, in_f, blk_cnt, t_col_ptr);
+        SP_CHECK_LAUNCH();
+    }
+    if ((s = sp::scan_counts(t_col_ptr, in_f, st))) return s;
+    if (out_f > 0 && nnz > 0 && in_f > 0) {
+        hipLaunchKernelGGL(k_csc_block_offsets, dim3((unsigned)sp::ceil_div(in_f, 256)), dim3(256), 0,
+                           st, blk_cnt, nblk, in_f, t_col_ptr);
+        SP_CHECK_LAUNCH();
+        hipLaunchKernelGGL(k_csc_fill, dim3((unsigned)nblk), dim3(64), (size_t)in_f * 4, st, row_ptr,
+                           col_idx, out_f, in_f, blk_cnt, t_row_idx, t_perm);
+        SP_CHECK_LAUNCH();
+    }
+    return SP_OK;
+}
+
+// --------------------------------------------------------------------------
+// Linear geometry.  G is In[ntok][ld] (only columns < ncols are read); the
+// SpMM output is Out[ntok][ldo]; the SDDMM stationary operand is D[ntok][ldd].
+// MODE 2 (fast): ld % 4 == 0, ncols % 64 == 0 and the operand spans < 2 GiB.
+//   Slabs are read with buffer loads whose per-thread offsets are fixed for
+//   the whole kernel and whose slab position is a scalar offset; the buffer
+//   range check returns zeros for rows past the last token.
+// MODE 1: ld % 4 == 0 otherwise; clamped 16-byte loads plus a validity mask.
+// MODE 0: general; clamped 4-byte loads plus a validity mask.
+template <int MODE>
+struct LinGeo {
+    const float *In;
+    int64_t ntok, ld, ncols;
+    float *Out;
+    int64_t ldo, nrows;
+    const float *D;
+    int64_t ldd;
+
+    struct Tok {
+        sp_i32x4 rsrc;
+        int voff;   // byte offset of this thread's first piece within a slab
+        int xsoff;  // float offset of this thread's first LDS element
+    };
+    // Slab pieces: 4096 float4, piece f = tid + NTHR*i; a wave instruction
+    // covers 16 tokens x 4 float4 (64-byte row segments) and the transposed
+    // LDS writes hit 64 distinct banks.  For thread (lane, wave w) and piece
+    // i: token t = (lane & 15) + 16w, float4 column qd = (lane >> 4) + 4i.
+    __device__ void tile_init(Tok &tk, int64_t t0, int lane) const {
+        const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int t = (lane & 15) + 16 * w;
+        if (MODE == 2) {
+            const int64_t rows_left = ntok - t0;  // >= 1
+            tk.rsrc = sp::make_rsrc(In + t0 * ld, (uint32_t)(rows_left * ld * 4));
+            tk.voff = (int)((t * ld + 4 * (lane >> 4)) * 4);
+        }
+        tk.xsoff = 4 * (lane >> 4) * TS + t;
+    }
+    __device__ uint32_t load_slab(float (&pf)[PF], const Tok &tk, int64_t t0, int64_t c0, int tid) const {
+        if (MODE == 2) {
+            const int soff = (int)(c0 * 4);
+#pragma unroll
+            for (int i = 0; i < PF / 4; ++i) {
+                const sp_f32x4 v = sp_raw_buffer_load_f32x4(tk.rsrc, tk.voff + 64 * i, soff, 0);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) pf[4 * i + e] = v[e];
+            }
+            return 0xffffffffu;
+        }
+        const int lane = tid & 63, w = tid >> 6;
+        uint32_t mask = 0;
+#pragma unroll
+        for (int i = 0; i < PF / 4; ++i) {
+            const int t = (lane & 15) + 16 * w;
+            const int qd = (lane >> 4) + 4 * i;
+            const int64_t gt = t0 + t, gc = c0 + 4 * qd;
+            const int64_t ct = gt < ntok ? gt : ntok - 1;
+            if (MODE == 1) {
+                const int64_t cc = gc < ncols ? gc : ncols - 4;
+                const float4 v = *reinterpret_cast<const float4 *>(In + ct * ld + cc);
+                pf[4 * i + 0] = v.x;
+                pf[4 * i + 1] = v.y;
+                pf[4 * i + 2] = v.z;
+                pf[4 * i + 3] = v.w;
+                if (gt < ntok && gc < ncols) mask |= 0xfu << (4 * i);
+            } else {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const int64_t ge = gc + e;
+                    pf[4 * i + e] = In[ct * ld + (ge < ncols ? ge : ncols - 1)];
+                    if (gt < ntok && ge < ncols) mask |= 1u << (4 * i + e);
+                }
+            }
+        }
+        return mask;
+    }
+    __device__ void write_slab(float *xs, const float (&pf)[PF], uint32_t mask, const Tok &tk, int) const {
+        float *x = xs + tk.xsoff;
+#pragma unroll
+        for (int i = 0; i < PF / 4; ++i)
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+                x[(16 * i + e) * TS] = (MODE == 2 || ((mask >> (4 * i + e)) & 1u)) ? pf[4 * i + e] : 0.f;
+    }
+
+    // Output tile through LDS (two halves of 128 tokens) so that global stores
+    // are full row segments of R floats.
+    template <int RW>
+    __device__ void store(float *ys, const float (&acc)[RW][4], const Tok &, int64_t t0, int64_t row0, int tid,
+                          int lane, int rw0) const {
+        constexpr int R = NW * RW, YS = R + 1;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();
+            if ((lane >> 5) == h) {
+                const int tl = 4 * (lane & 31);
+#pragma unroll
+                for (int r = 0; r < RW; ++r)
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) ys[(tl + k) * YS + rw0 + r] = acc[r][k];
+            }
+            __syncthreads();
+            for (int e = tid; e < 128 * R; e += NTHR) {
+                const int tl = e / R, r = e % R;
+                const int64_t gt = t0 + 128 * h + tl, gr = row0 + r;
+                if (gt < ntok && gr < nrows) Out[gt * ldo + gr] = ys[tl * YS + r];
+            }
+        }
+    }
+
+    // D[t0 + 4*lane + k][row0 + rw0 + r] -> d[r][k], through LDS in two halves.
+    template <int RW>
+    __device__ void load_d(float *ys, float (&d)[RW][4], const Tok &, int64_t t0, int64_t row0, int tid, int lane,
+                           int rw0) const {
+        constexpr int R = NW * RW, YS = R + 1;
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();
+            for (int e = tid; e < 128 * R; e += NTHR) {
+                const int tl = e / R, r = e % R;
+                const int64_t gt = t0 + 128 * h + tl, gr = row0 + r;
+                ys[tl * YS + r] = (gt < ntok && gr < nrows) ? D[gt * ldd + gr] : 0.f;
+            }
+            __syncthreads();
+            if ((lane >> 5) == h) {
+                const int tl = 4 * (lane & 31);
+#pragma unroll
+                for (int r = 0; r < RW; ++r)
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) d[r][k] = ys[(tl + k) * YS + rw0 + r];
+            }
+        }
+    }
+};
+
+// Plan layout: a pure function of (in_f, out_f, nnz).
+struct PlanLayout {
+    int32_t *t_col_ptr, *t_row_idx, *t_perm;
+    spt::Tiling A, Bt;  // A: rows = out_f (forward, weight gradient); Bt: rows = in_f (input gradient)
+    int32_t *cnt;       // scratch [max(out_f*KA, in_f*KB)]
+    int32_t *blk_cnt;   // transpose scratch [ceil(out_f/TR_BLK) * in_f]
+    size_t bytes;
+};
+
+PlanLayout plan_layout(const void *base, int64_t in_f, int64_t out_f, int64_t nnz) {
+    sp::Carve c(const_cast<void *>(base));
+    PlanLayout L;
+    L.t_col_ptr = c.take<int32_t>(in_f + 1);
+    L.t_row_idx = c.take<int32_t>(nnz);
+    L.t_perm = c.take<int32_t>(nnz);
+    spt::tiling_layout(c, L.A, out_f, in_f, nnz);
+    spt::tiling_layout(c, L.Bt, in_f, out_f, nnz);
+    L.cnt = c.take<int32_t>(std::max(out_f * L.A.K, in_f * L.Bt.K));
+    L.blk_cnt = c.take<int32_t>(sp::ceil_div(out_f, TR_BLK) * in_f);
+    L.bytes = c.off;
+    return L;
+}
+
+bool bad_dims(int64_t a, int64_t b, int64_t nnz) {
+    return a < 0 || b < 0 || nnz < 0 || nnz > 0x7fffffffLL || a > 0x7fffffffLL || b > 0x7fffffffLL ||
+           (a > 0 && b > 0 && nnz > a * b) || ((a == 0 || b == 0) && nnz > 0);
+}
+
+int64_t ntiles_of(int64_t ntok) { return sp::ceil_div(ntok, T); }
+
+// Staging mode of a [ntok][ncols] gathered operand (see LinGeo).
+int lin_mode(int64_t ntok, int64_t ncols) {
+    if (ncols % 4 != 0) return 0;
+    if (ncols % C == 0 && ntok * ncols * 4 < 0x7fffffffLL) return 2;
+    return 1;
+}
+
+template <int MODE>
+sp_status spmm_launch_t(const spt::Tiling &t, const LinGeo<MODE> &geo, const float *vals, hipStream_t st) {
+    const int64_t ntiles = ntiles_of(geo.ntok);
+    const int64_t nwg = t.P * ntiles;
+    if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    if (t.R == 128)
+        hipLaunchKernelGGL((spt::k_spmm<8, LinGeo<MODE>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals,
+                           t.view(), (int)ntiles);
+    else
+        hipLaunchKernelGGL((spt::k_spmm<4, LinGeo<MODE>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals,
+                           t.view(), (int)ntiles);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+__global__ void k_zero_f32(float *p, int64_t n);
+
+// Out[ntok][nrows] = sparse product over tiling t of In[ntok][ncols].
+sp_status spmm_launch(const spt::Tiling &t, const float *In, int64_t ntok, int64_t ncols, float *Out,
+                      int64_t nrows, const float *vals, int64_t nnz, hipStream_t st) {
+    if (ntok == 0 || nrows == 0) return SP_OK;
+    if (nnz == 0) {  // no stored entries: the product is zero
+        hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)std::min<int64_t>(sp::ceil_div(ntok * nrows, 256), 4096)),
+                           dim3(256), 0, st, Out, ntok * nrows);
+        SP_CHECK_LAUNCH();
+        return SP_OK;
+    }
+    const int mode = lin_mode(ntok, ncols);
+    if (mode == 2)
+        return spmm_launch_t<2>(t, LinGeo<2>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+    if (mode == 1)
+        return spmm_launch_t<1>(t, LinGeo<1>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+    return spmm_launch_t<0>(t, LinGeo<0>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+}
+
+__global__ void k_zero_f32(float *p, int64_t n) {  // definition
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) p[i] = 0.f;
+}
+
+}  // namespace
+
+// ==========================================================================
+// C ABI
+
+extern "C" sp_status sp_linear_encode_rows(int64_t out_f, int64_t in_f, const uint8_t *mask, int32_t *row_ptr,
+                                           void *stream) {
+    if (out_f < 0 || in_f < 0 || !row_ptr || (out_f * in_f > 0 && !mask)) return SP_ERR_INVALID_ARG;
+    hipStream_t st = (hipStream_t)stream;
+    sp_status s;
+    if ((s = sp::fill_i32(row_ptr, out_f + 1, 0, st))) return s;
+    if (out_f > 0 && in_f > 0) {
+        hipLaunchKernelGGL(k_encode_rows, dim3((unsigned)sp::ceil_div(out_f, 4)), dim3(256), 0, st, mask, out_f,
+                           in_f, row_ptr);
+        SP_CHECK_LAUNCH();
+    }
+    return sp::scan_counts(row_ptr, out_f, st);
+}
+
+extern "C" sp_status sp_linear_encode_fill(int64_t out_f, int64_t in_f, const uint8_t *mask, const float *W,
+                                           const int32_t *row_ptr, int32_t *col_idx, float *vals, void *stream) {
+    if (out_f < 0 || in_f < 0 || !row_ptr) return SP_ERR_INVALID_ARG;
+    if (out_f * in_f > 0 && (!mask || !W || !col_idx || !vals)) return SP_ERR_INVALID_ARG;
+    if (out_f == 0 || in_f == 0) return SP_OK;
+    hipLaunchKernelGGL(k_encode_fill, dim3((unsigned)sp::ceil_div(out_f, 4)), dim3(256), 0, (hipStream_t)stream,
+                       mask, W, out_f, in_f, row_ptr, col_idx, vals);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+extern "C" sp_status sp_linear_transpose_ws(int64_t in_f, int64_t out_f, int64_t nnz, size_t *bytes) {
+    if (!bytes || bad_dims(in_f, out_f, nnz)) return SP_ERR_INVALID_ARG;
+    *bytes = sp::align256((size_t)sp::ceil_div(out_f, TR_BLK) * (size_t)std::max<int64_t>(in_f, 1) * 4);
+    return SP_OK;
+}
+
+extern "C" sp_status sp_linear_transpose(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
+                                         int64_t nnz, int32_t *t_col_ptr, int32_t *t_row_idx, int32_t *t_perm,
+                                         void *scratch, size_t scratch_bytes, void *stream) {
+    if (bad_dims(in_f, out_f, nnz) || !row_ptr || !t_col_ptr) return SP_ERR_INVALID_ARG;
+    if (nnz > 0 && (!col_idx || !t_row_idx || !t_perm)) return SP_ERR_INVALID_ARG;
+    if (in_f * 4 > 160 * 1024) return SP_ERR_UNSUPPORTED;
+    size_t need;
+    sp_linear_transpose_ws(in_f, out_f, nnz, &need);
+    if (!scratch || scratch_bytes < need) return SP_ERR_WORKSPACE;
+    return csc_build(in_f, out_f, row_ptr, col_idx, nnz, t_col_ptr, t_row_idx, t_perm, (int32_t *)scratch,
+                     (hipStream_t)stream);
+}
+
+extern "C" sp_status sp_linear_plan_bytes(int64_t in_f, int64_t out_f, int64_t nnz, size_t *bytes) {
+    if (!bytes || bad_dims(in_f, out_f, nnz)) return SP_ERR_INVALID_ARG;
+    *bytes = plan_layout(nullptr, in_f, out_f, nnz).bytes;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_linear_plan(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
+                                    int64_t nnz, void *plan, size_t plan_bytes, void *stream) {
+    if (bad_dims(in_f, out_f, nnz) || !row_ptr || !plan || (nnz > 0 && !col_idx)) return SP_ERR_INVALID_ARG;
+    if (in_f * 4 > 160 * 1024 || in_f > 65535 * C) return SP_ERR_UNSUPPORTED;
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    if (plan_bytes < L.bytes) return SP_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    sp_status s;
+    if ((s = csc_build(in_f, out_f, row_ptr, col_idx, nnz, L.t_col_ptr, L.t_row_idx, L.t_perm, L.blk_cnt, st)))
+        return s;
+    if ((s = spt::tiling_build(L.A, row_ptr, col_idx, nullptr, L.cnt, st))) return s;
+    return spt::tiling_build(L.Bt, L.t_col_ptr, L.t_row_idx, L.t_perm, L.cnt, st);
+}
+
+extern "C" sp_status sp_linear_plan_csc(const void *plan, int64_t in_f, int64_t out_f, int64_t nnz,
+                                        int32_t *t_col_ptr, int32_t *t_row_idx, int32_t *t_perm, void *stream) {
+    if (!plan || bad_dims(in_f, out_f, nnz) || !t_col_ptr || (nnz > 0 && (!t_row_idx || !t_perm)))
+        return SP_ERR_INVALID_ARG;
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    hipStream_t st = (hipStream_t)stream;
+    if (hipMemcpyAsync(t_col_ptr, L.t_col_ptr, (in_f + 1) * 4, hipMemcpyDeviceToDevice, st) != hipSuccess)
+        return SP_ERR_HIP;
+    if (nnz > 0) {
+        if (hipMemcpyAsync(t_row_idx, L.t_row_idx, nnz * 4, hipMemcpyDeviceToDevice, st) != hipSuccess)
+            return SP_ERR_HIP;
+        if (hipMemcpyAsync(t_perm, L.t_perm, nnz * 4, hipMemcpyDeviceToDevice, st) != hipSuccess) return SP_ERR_HIP;
+    }
+    return SP_OK;
+}
+
+extern "C" sp_status sp_linear_fwd(const float *X, int64_t B, int64_t in_f, int64_t out_f, const float *vals,
+                                   int64_t nnz, const void *plan, float *Y, void *stream) {
+    if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
+    if ((B * out_f > 0 && !Y) || (B * in_f > 0 && !X) || (nnz > 0 && !vals)) return SP_ERR_INVALID_ARG;
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    return spmm_launch(L.A, X, B, in_f, Y, out_f, vals, nnz, (hipStream_t)stream);
+}
+
+extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f, const float *vals,
+                                         int64_t nnz, const void *plan, float *dX, void *stream) {
+    if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
+    if ((B * in_f > 0 && !dX) || (B * out_f > 0 && !dY) || (nnz > 0 && !vals)) return SP_ERR_INVALID_ARG;
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    return spmm_launch(L.Bt, dY, B, out_f, dX, in_f, vals, nnz, (hipStream_t)stream);
+}
+
+extern "C" sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f, int64_t nnz, size_t *bytes) {
+    if (!bytes || B < 0 || bad_dims(in_f, out_f, nnz)) return SP_ERR_INVALID_ARG;
+    *bytes = nnz > 0 ? sp::align256((size_t)ntiles_of(B) * (size_t)spt::padded_cap(nnz) * 4) : 0;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64_t B, int64_t in_f, int64_t out_f,
+                                          int64_t nnz, const void *plan, float *dW, void *workspace, size_t ws_bytes,
+                                          void *stream) {
+    if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
+    if (nnz > 0 && !dW) return SP_ERR_INVALID_ARG;
+    if (B > 0 && nnz > 0 && (!dY || !X)) return SP_ERR_INVALID_ARG;
+    size_t need;
+    sp_linear_bwd_weight_ws(B, in_f, out_f, nnz, &need);
+    if (nnz > 0 && B > 0 && (!workspace || ws_bytes < need)) return SP_ERR_WORKSPACE;
+    if (nnz == 0) return SP_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (B == 0) {
+        hipLaunchKernelGGL(k_zero_f32, dim3((unsigned)std::min<int64_t>(sp::ceil_div(nnz, 256), 4096)), dim3(256),
+                           0, st, dW, nnz);
+        SP_CHECK_LAUNCH();
+        return SP_OK;
+    }
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    const int64_t ntiles = ntiles_of(B);
+    const int64_t nwg = L.A.P * ntiles;
+    if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    float *part = (float *)workspace;
+    auto launch = [&](auto geo) {
+        using G = decltype(geo);
+        if (L.A.R == 128)
+            hipLaunchKernelGGL((spt::k_sddmm<8, G>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, L.A.view(),
+                               (int)ntiles, L.A.cap, part);
+        else
+            hipLaunchKernelGGL((spt::k_sddmm<4, G>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, L.A.view(),
+                               (int)ntiles, L.A.cap, part);
+    };
+    const int mode = lin_mode(B, in_f);
+    if (mode == 2)
+        launch(LinGeo<2>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+    else if (mode == 1)
+        launch(LinGeo<1>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+    else
+        launch(LinGeo<0>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+    SP_CHECK_LAUNCH();
+    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, st);
+}
+
+extern "C" sp_status sp_linear_validate(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
+                                        int64_t nnz) {
+    if (bad_dims(in_f, out_f, nnz) || !row_ptr || (nnz > 0 && !col_idx)) return SP_ERR_INVALID_ARG;
+    if (row_ptr[0] != 0 || row_ptr[out_f] != nnz) return SP_ERR_INVALID_ARG;
+    for (int64_t i = 0; i < out_f; ++i) {
+        if (row_ptr[i + 1] < row_ptr[i]) return SP_ERR_INVALID_ARG;
+        for (int32_t j = row_ptr[i]; j < row_ptr[i + 1]; ++j) {
+            if (col_idx[j] < 0 || col_idx[j] >= in_f) return SP_ERR_INVALID_ARG;
+            if (j > row_ptr[i] && col_idx[j] <= col_idx[j - 1]) return SP_ERR_INVALID_ARG;
+        }
+    }
+    return SP_OK;
+}

@@ -1,0 +1,236 @@
+"""GPU parity of the sparse linear passes against the CPU oracle.
+
+Structure outputs (CSR encoding, CSC view) must be bit-exact; values must
+satisfy |gpu - oracle| <= 1e-5 * abssum elementwise, with exact zeros where
+no stored weight contributes (abssum == 0).  1e-5 is the tolerance the
+method's fp32 arithmetic is held to; fp32 accumulation over n terms in any
+order stays within ~n * 2^-24 * abssum, far below it for every size here.
+"""
+import sys
+
+import numpy as np
+import pytest
+
+from synth import linear_layer
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-5
+
+
+def _say(msg):
+    print("[gpu-linear] " + msg, flush=True)
+    sys.stdout.flush()
+
+
+@pytest.fixture(scope="module")
+def sp():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2302_04852_amd as m
+    return m
+
+
+def assert_parity(gpu, ref, abssum, what):
+    gpu = np.asarray(gpu, np.float64)
+    assert gpu.shape == ref.shape, what
+    err = np.abs(gpu - ref)
+    bound = TOL * abssum
+    zero = abssum == 0
+    assert np.all(gpu[zero] == 0), what + ": nonzero output where no term contributes"
+    bad = err > bound
+    assert not bad.any(), "%s: %d violations, worst excess %g" % (what, int(bad.sum()), float((err - bound).max()))
+
+
+class GpuLayer:
+    """Product-side structure for one sparse linear layer: encode on the GPU,
+    check the encoding against the oracle's, build the plan."""
+
+    def __init__(self, sp, orc, mask, W):
+        import torch
+        self.sp = sp
+        out_f, in_f = mask.shape
+        self.out_f, self.in_f = out_f, in_f
+        dev = torch.device("cuda")
+        m = torch.from_numpy(np.ascontiguousarray(mask)).to(dev)
+        w = torch.from_numpy(np.ascontiguousarray(W)).to(dev)
+        self.row_ptr = torch.empty(out_f + 1, dtype=torch.int32, device=dev)
+        sp.sp_linear_encode_rows(out_f, in_f, m, self.row_ptr)
+        nnz = int(self.row_ptr[-1].item())
+        self.nnz = nnz
+        self.col_idx = torch.empty(max(nnz, 1), dtype=torch.int32, device=dev)
+        self.vals = torch.empty(max(nnz, 1), dtype=torch.float32, device=dev)
+        sp.sp_linear_encode_fill(out_f, in_f, m, w, self.row_ptr, self.col_idx, self.vals)
+        o_rp, o_ci, o_v = orc.linear_encode(mask, W)
+        np.testing.assert_array_equal(self.row_ptr.cpu().numpy(), o_rp)
+        np.testing.assert_array_equal(self.col_idx.cpu().numpy()[:nnz], o_ci)
+        np.testing.assert_array_equal(self.vals.cpu().numpy()[:nnz], o_v)
+        self.o_rp, self.o_ci, self.o_v = o_rp, o_ci, o_v
+        self.plan = torch.empty(sp.sp_linear_plan_bytes(in_f, out_f, nnz), dtype=torch.uint8, device=dev)
+        sp.sp_linear_plan(in_f, out_f, self.row_ptr, self.col_idx, nnz, self.plan)
+
+    def fwd(self, X):
+        import torch
+        Y = torch.full((X.shape[0], self.out_f), float("nan"), device="cuda")
+        self.sp.sp_linear_fwd(X, X.shape[0], self.in_f, self.out_f, self.vals, self.nnz, self.plan, Y)
+        return Y
+
+    def bwd_input(self, dY):
+        import torch
+        dX = torch.full((dY.shape[0], self.in_f), float("nan"), device="cuda")
+        self.sp.sp_linear_bwd_input(dY, dY.shape[0], self.in_f, self.out_f, self.vals, self.nnz, self.plan, dX)
+        return dX
+
+    def bwd_weight(self, dY, X):
+        import torch
+        B = X.shape[0]
+        ws = torch.empty(self.sp.sp_linear_bwd_weight_ws(B, self.in_f, self.out_f, self.nnz),
+                         dtype=torch.uint8, device="cuda")
+        dW = torch.full((max(self.nnz, 1),), float("nan"), device="cuda")
+        self.sp.sp_linear_bwd_weight(dY, X, B, self.in_f, self.out_f, self.nnz, self.plan, dW, ws)
+        return dW[:self.nnz]
+
+
+def _run_all(sp, orc, mask, W, X, dY, name):
+    import torch
+    _say("case %s: out=%d in=%d B=%d nnz=%d" % (name, mask.shape[0], mask.shape[1], X.shape[0], int(mask.sum())))
+    L = GpuLayer(sp, orc, mask, W)
+    Xd = torch.from_numpy(X).cuda()
+    dYd = torch.from_numpy(dY).cuda()
+    Y = L.fwd(Xd)
+    dX = L.bwd_input(dYd)
+    dW = L.bwd_weight(dYd, Xd)
+    torch.cuda.synchronize()
+    Yr, Ya = orc.linear_fwd(X, L.o_rp, L.o_ci, L.o_v, mask.shape[0])
+    assert_parity(Y.cpu().numpy(), Yr, Ya, name + " fwd")
+    dXr, dXa = orc.linear_bwd_input(dY, L.o_rp, L.o_ci, L.o_v, mask.shape[1])
+    assert_parity(dX.cpu().numpy(), dXr, dXa, name + " bwd_input")
+    dWr, dWa = orc.linear_bwd_weight(dY, X, L.o_rp, L.o_ci)
+    assert_parity(dW.cpu().numpy(), dWr, dWa, name + " bwd_weight")
+    return L, Y, dX, dW
+
+
+def test_plan_csc_and_transpose_bit_exact(sp, orc):
+    import torch
+    d = linear_layer(11, 300, 200, 1, 0.9)
+    L = GpuLayer(sp, orc, d["mask"], d["W"])
+    t_cp, t_ri, t_pm = orc.linear_transpose(200, 300, L.o_rp, L.o_ci)
+    a = torch.empty(201, dtype=torch.int32, device="cuda")
+    b = torch.empty(L.nnz, dtype=torch.int32, device="cuda")
+    c = torch.empty(L.nnz, dtype=torch.int32, device="cuda")
+    sp.sp_linear_plan_csc(L.plan, 200, 300, L.nnz, a, b, c)
+    np.testing.assert_array_equal(a.cpu().numpy(), t_cp)
+    np.testing.assert_array_equal(b.cpu().numpy(), t_ri)
+    np.testing.assert_array_equal(c.cpu().numpy(), t_pm)
+    scratch = torch.empty(sp.sp_linear_transpose_ws(200, 300, L.nnz), dtype=torch.uint8, device="cuda")
+    a.fill_(-1); b.fill_(-1); c.fill_(-1)
+    sp.sp_linear_transpose(200, 300, L.row_ptr, L.col_idx, L.nnz, a, b, c, scratch)
+    np.testing.assert_array_equal(a.cpu().numpy(), t_cp)
+    np.testing.assert_array_equal(b.cpu().numpy(), t_ri)
+    np.testing.assert_array_equal(c.cpu().numpy(), t_pm)
+
+
+def test_small_layer_seed0(sp, orc):
+    """256x256 at 90% sparsity, 16 tokens, seed 0."""
+    d = linear_layer(0, 256, 256, 16, 0.90)
+    _run_all(sp, orc, d["mask"], d["W"], d["X"], d["dY"], "256x256@90 B16")
+
+
+@pytest.mark.parametrize("out_f,in_f,B,density", [
+    (200, 300, 300, 0.1),     # ragged in every dimension, several tiles
+    (129, 65, 257, 0.3),      # one row/column/token past a tile boundary
+    (70, 130, 513, 0.05),
+    (5, 7, 3, 1.0),           # fully dense, tiny
+    (300, 150, 100, 1.0),     # dense: several staging rounds per tile
+    (1, 1, 1, 1.0),
+    (64, 33, 9, 0.5),         # in_f not a multiple of 4 (scalar staging path)
+])
+def test_ragged_shapes(sp, orc, out_f, in_f, B, density):
+    rng = np.random.default_rng(out_f * 7 + in_f * 3 + B)
+    mask = (rng.random((out_f, in_f)) < density).astype(np.uint8)
+    W = (rng.standard_normal((out_f, in_f)) * 0.05).astype(np.float32) * mask
+    X = rng.standard_normal((B, in_f)).astype(np.float32)
+    dY = rng.standard_normal((B, out_f)).astype(np.float32)
+    _run_all(sp, orc, mask, W.astype(np.float32), X, dY, "ragged %dx%d B%d d%.2f" % (out_f, in_f, B, density))
+
+
+def test_edge_patterns(sp, orc):
+    rng = np.random.default_rng(5)
+    out_f, in_f, B = 260, 190, 70
+    mask = (rng.random((out_f, in_f)) < 0.05).astype(np.uint8)
+    mask[7, :] = 1                 # all-dense row
+    mask[9, :] = 0                 # empty row
+    mask[:, 11] = 0                # empty column
+    mask[:, 150] = 1               # all-dense column
+    mask[200, :] = 0
+    mask[200, ::2] = 1             # skewed: one long row
+    W = (rng.standard_normal((out_f, in_f)) * 0.05).astype(np.float32) * mask
+    W[7, 3] = 0.0                  # stored zero
+    X = rng.standard_normal((B, in_f)).astype(np.float32)
+    dY = rng.standard_normal((B, out_f)).astype(np.float32)
+    _run_all(sp, orc, mask, W.astype(np.float32), X, dY, "edge patterns")
+
+
+def test_skewed_half_in_one_row(sp, orc):
+    rng = np.random.default_rng(6)
+    out_f, in_f, B = 512, 1024, 64
+    mask = (rng.random((out_f, in_f)) < 0.002).astype(np.uint8)
+    mask[100, :] = 1               # one row holds ~half of all entries
+    W = (rng.standard_normal((out_f, in_f)) * 0.05).astype(np.float32) * mask
+    X = rng.standard_normal((B, in_f)).astype(np.float32)
+    dY = rng.standard_normal((B, out_f)).astype(np.float32)
+    _run_all(sp, orc, mask, W.astype(np.float32), X, dY, "skewed row")
+
+
+def test_empty_pattern_writes_zeros(sp, orc):
+    import torch
+    mask = np.zeros((40, 30), np.uint8)
+    W = np.zeros((40, 30), np.float32)
+    L = GpuLayer(sp, orc, mask, W)
+    assert L.nnz == 0
+    X = torch.randn(20, 30, device="cuda")
+    dY = torch.randn(20, 40, device="cuda")
+    assert torch.all(L.fwd(X) == 0)
+    assert torch.all(L.bwd_input(dY) == 0)
+    assert L.bwd_weight(dY, X).numel() == 0
+
+
+def test_deterministic(sp, orc):
+    import torch
+    d = linear_layer(3, 384, 256, 700, 0.9)
+    L = GpuLayer(sp, orc, d["mask"], d["W"])
+    X = torch.from_numpy(d["X"]).cuda()
+    dY = torch.from_numpy(d["dY"]).cuda()
+    a = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
+    b = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
+def test_error_paths(sp, orc):
+    import torch
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_plan_bytes(-1, 4, 0)
+    assert e.value.status == sp.SP_ERR_INVALID_ARG
+    d = linear_layer(1, 32, 16, 8, 0.5)
+    L = GpuLayer(sp, orc, d["mask"], d["W"])
+    X = torch.from_numpy(d["X"]).cuda()
+    dY = torch.from_numpy(d["dY"]).cuda()
+    small = torch.empty(4, dtype=torch.uint8, device="cuda")
+    dW = torch.empty(L.nnz, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_bwd_weight(dY, X, 8, 16, 32, L.nnz, L.plan, dW, small)
+    assert e.value.status == sp.SP_ERR_WORKSPACE
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_plan(16, 32, L.row_ptr, L.col_idx, L.nnz, small)
+    assert e.value.status == sp.SP_ERR_WORKSPACE
+
+
+@pytest.mark.parametrize("layer", [0, 1])
+def test_ffn_layer_full_size(sp, orc, layer):
+    """The FFN pair at its full size: 8192 tokens, 768<->3072, 95% sparse,
+    checked element by element against the oracle over all outputs."""
+    out_f, in_f = (3072, 768) if layer == 0 else (768, 3072)
+    d = linear_layer(1000 + layer, out_f, in_f, 8192, 0.95)
+    _run_all(sp, orc, d["mask"], d["W"], d["X"], d["dY"], "ffn W%d full" % (layer + 1))
