@@ -206,43 +206,52 @@ sp_status sp_conv_encode_fill(int64_t OC, int64_t IC, int32_t KH, int32_t KW,
  * [t_ic_ptr[ic], t_ic_ptr[ic+1]) list the stored entries with that input
  * channel in ascending (oc, x, y) order; t_oc holds the output channel and
  * t_perm the index into w_x/w_y/w_vals.  Outputs: t_ic_ptr [IC+1],
- * t_oc [nnz], t_perm [nnz].  Built once per mask; bit-exact. */
+ * t_oc [nnz], t_perm [nnz].  Bit-exact and deterministic. */
 sp_status sp_conv_transpose(int64_t OC, int64_t IC, const int32_t *w_oc,
                             const int16_t *w_ic, int64_t nnz, int32_t *t_ic_ptr,
                             int32_t *t_oc, int32_t *t_perm, void *stream);
 
+/* Plan: the weight pattern prepared once (as for linear layers).  Opaque
+ * device buffer of sp_conv_plan_bytes() bytes, built by sp_conv_plan() from
+ * the five-array pattern.  It holds the input-channel-major view and, for
+ * the forward/weight-gradient and the input-gradient orientations, the
+ * stored entries regrouped into tiles of output (input) channels x 64
+ * (channel, tap) columns.  It depends only on OC, IC, KH, KW and the
+ * pattern: it stays valid for any batch, spatial size, stride and padding,
+ * and for any values. */
+sp_status sp_conv_plan_bytes(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
+sp_status sp_conv_plan(const sp_conv_shape *s, const int32_t *w_oc, const int16_t *w_ic,
+                       const uint8_t *w_x, const uint8_t *w_y, int64_t nnz, void *plan,
+                       size_t plan_bytes, void *stream);
+
 /* Forward pass, Eq. 3 with stride and padding:
  *   Y[b,oc,p,q] = sum over entries si of oc of
  *                 w_vals[si] * X[b, ic(si), p*sh + w_x[si] - ph, q*sw + w_y[si] - pw]
- * (taps in the zero padding contribute nothing).  Y: out [B][OC][OH][OW]. */
-sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const int32_t *w_oc,
-                      const int16_t *w_ic, const uint8_t *w_x, const uint8_t *w_y,
-                      const float *w_vals, int64_t nnz, float *Y, void *stream);
-
-/* Workspace bytes needed by sp_conv_bwd_input (host). */
-sp_status sp_conv_bwd_input_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
+ * (taps in the zero padding contribute nothing).  Computed as an implicit
+ * im2col product: the (channel, tap) columns of the unfolded input are
+ * gathered straight from X into LDS, never materialised.
+ * X: [B][IC][H][W]; w_vals in the format's order; Y: out [B][OC][OH][OW]. */
+sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const float *w_vals,
+                      int64_t nnz, const void *plan, float *Y, void *stream);
 
 /* Input gradient, Eq. 4 with stride and padding: every term of Eq. 3 that
  * reads X[b,ic,m,n] contributes w_vals[si] * dY[b,oc,p,q] to dX[b,ic,m,n].
- * Computed per input channel over the ic-major view (one writer per dX
- * element, no atomics).  t_* from sp_conv_transpose.  dX: out [B][IC][H][W]. */
+ * Computed per input channel over the input-channel-major tiles (one writer
+ * per dX element, no atomics).  dY: [B][OC][OH][OW]; dX: out [B][IC][H][W]. */
 sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s,
-                            const uint8_t *w_x, const uint8_t *w_y,
-                            const float *w_vals, const int32_t *t_ic_ptr,
-                            const int32_t *t_oc, const int32_t *t_perm, int64_t nnz,
-                            float *dX, void *workspace, size_t ws_bytes, void *stream);
+                            const float *w_vals, int64_t nnz, const void *plan,
+                            float *dX, void *stream);
 
 /* Workspace bytes needed by sp_conv_bwd_weight (host). */
 sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
 
 /* Weight gradient, Eq. 5 with stride and padding, only for stored entries:
  *   dW[si] = sum_{b,p,q} dY[b,oc,p,q] * X[b, ic, p*sh + x - ph, q*sw + y - pw]
- * in the format's entry order.  Deterministic split reduction over
- * (b, p, q).  dW: out [nnz]. */
+ * in the format's entry order.  Deterministic split reduction over the
+ * output pixels.  dW: out [nnz]; workspace: sp_conv_bwd_weight_ws() bytes. */
 sp_status sp_conv_bwd_weight(const float *dY, const float *X, const sp_conv_shape *s,
-                             const int32_t *w_oc, const int16_t *w_ic,
-                             const uint8_t *w_x, const uint8_t *w_y, int64_t nnz,
-                             float *dW, void *workspace, size_t ws_bytes, void *stream);
+                             int64_t nnz, const void *plan, float *dW, void *workspace,
+                             size_t ws_bytes, void *stream);
 
 /* Host.  Structural check of a five-array pattern held in HOST memory. */
 sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW,

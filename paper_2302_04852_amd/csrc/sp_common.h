@@ -21,6 +21,8 @@ typedef int sp_i32x4 __attribute__((ext_vector_type(4)));
 typedef float sp_f32x4 __attribute__((ext_vector_type(4)));
 __device__ sp_f32x4 sp_raw_buffer_load_f32x4(sp_i32x4 rsrc, int voffset, int soffset, int aux) __asm(
     "llvm.amdgcn.raw.buffer.load.v4f32");
+__device__ float sp_raw_buffer_load_f32(sp_i32x4 rsrc, int voffset, int soffset, int aux) __asm(
+    "llvm.amdgcn.raw.buffer.load.f32");
 
 namespace sp {
 
@@ -55,9 +57,6 @@ struct Carve {
 // each with its own L2.  Remap so that each XCD receives a contiguous range
 // of logical work items (neighbouring tiles share their L2).
 __device__ inline int xcd_remap(int b, int n) {
-#if defined(SP_NO_XCD_REMAP)
-    return b;
-#endif
     const int per = n / 8, rem = n % 8;
     const int xcd = b % 8, k = b / 8;
     return (xcd < rem) ? xcd * (per + 1) + k : rem * (per + 1) + (xcd - rem) * per + k;

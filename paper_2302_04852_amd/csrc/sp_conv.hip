@@ -1,0 +1,628 @@
+// Sparse convolutions on gfx950 (SparseProp Sec. 3.3): encoders of the
+// five-array format, its input-channel-major view, the tiled plan, and the
+// three passes -- forward (Eq. 3), input gradient (Eq. 4) and weight gradient
+// at the stored entries (Eq. 5) -- with stride and zero padding.
+//
+// Each pass is one of the two tiled products of sp_tiled.h over an implicit
+// im2col operand.  A column of that operand is a (channel, tap) pair
+// col = ch*KH*KW + x*KW + y, a token is one pixel of one image:
+//   forward, weight gradient: rows = output channels, columns = (ic, tap),
+//     tokens = output pixels (b, p, q), G[t][col] = X[b, ic, p*sh+x-ph, q*sw+y-pw];
+//   input gradient: rows = input channels, columns = (oc, tap) from the
+//     input-channel-major view, tokens = input pixels (b, m, n),
+//     G[t][col] = dY[b, oc, (m+ph-x)/sh, (n+pw-y)/sw] where that divides
+//     exactly and lies inside dY, 0 elsewhere.
+// Within a row (channel) the format's (channel, x, y) order is exactly the
+// ascending column order, so the format itself is the CSR of the forward
+// tiling.  The gather uses raw buffer loads: an element outside the image
+// (zero padding), past the last token or past the last column gets an
+// offset beyond the buffer's range and loads as 0, so staging has no
+// branches.  This requires every activation tensor to span less than 2 GiB.
+#include "sp_tiled.h"
+
+namespace {
+
+using spt::C;
+using spt::NTHR;
+using spt::NW;
+using spt::PF;
+using spt::T;
+using spt::TS;
+
+constexpr int OOB = 0x7ffffff0;       // byte offset beyond any accepted buffer range
+constexpr int TOK_INVALID = -(1 << 28);  // spatial origin of tokens past the end
+constexpr int YS = 132;               // LDS stride (floats) of one row of 128 tokens
+constexpr int64_t MAX_BYTES = 0x7fff0000LL;
+
+// --------------------------------------------------------------------------
+// Encoders: dense pattern [OC][IC][KH][KW] -> five arrays.  One wave per
+// output channel; lanes take 64 input channels at a time.
+
+__global__ __launch_bounds__(256) void k_conv_encode_rows(const uint8_t *__restrict__ mask, int64_t OC, int64_t IC,
+                                                          int KK, int32_t *__restrict__ w_oc,
+                                                          int16_t *__restrict__ w_ic) {
+    const int lane = threadIdx.x & 63;
+    const int64_t oc = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (oc >= OC) return;
+    int carry = 0;
+    for (int64_t ic0 = 0; ic0 < IC; ic0 += 64) {
+        const int64_t ic = ic0 + lane;
+        int cnt = 0;
+        if (ic < IC) {
+            const uint8_t *m = mask + (oc * IC + ic) * KK;
+            for (int t = 0; t < KK; ++t) cnt += (m[t] != 0);
+        }
+        int incl = cnt;
+        for (int d = 1; d < 64; d <<= 1) {
+            const int u = __shfl_up(incl, d, 64);
+            if (lane >= d) incl += u;
+        }
+        if (ic < IC) w_ic[oc * (IC + 1) + ic] = (int16_t)(carry + incl - cnt);
+        carry += __shfl(incl, 63, 64);
+    }
+    if (lane == 0) {
+        w_ic[oc * (IC + 1) + IC] = (int16_t)carry;
+        w_oc[oc + 1] = carry;
+    }
+}
+
+__global__ __launch_bounds__(256) void k_conv_encode_fill(const uint8_t *__restrict__ mask,
+                                                          const float *__restrict__ W, int64_t OC, int64_t IC,
+                                                          int KH, int KW, const int32_t *__restrict__ w_oc,
+                                                          const int16_t *__restrict__ w_ic, uint8_t *__restrict__ w_x,
+                                                          uint8_t *__restrict__ w_y, float *__restrict__ w_vals) {
+    const int lane = threadIdx.x & 63;
+    const int64_t oc = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (oc >= OC) return;
+    const int KK = KH * KW;
+    for (int64_t ic = lane; ic < IC; ic += 64) {
+        int32_t pos = w_oc[oc] + w_ic[oc * (IC + 1) + ic];
+        const int64_t p0 = (oc * IC + ic) * KK;
+        for (int x = 0; x < KH; ++x)
+            for (int y = 0; y < KW; ++y) {
+                const int64_t p = p0 + x * KW + y;
+                if (mask[p]) {
+                    w_x[pos] = (uint8_t)x;
+                    w_y[pos] = (uint8_t)y;
+                    w_vals[pos] = W[p];
+                    ++pos;
+                }
+            }
+    }
+}
+
+// --------------------------------------------------------------------------
+// Input-channel-major view.  One thread per input channel walks the output
+// channels in order, so each channel's list is stable by (oc, x, y).
+
+__device__ inline int32_t run_begin(const int32_t *w_oc, const int16_t *w_ic, int64_t IC, int64_t oc, int64_t ic) {
+    return w_oc[oc] + w_ic[oc * (IC + 1) + ic];
+}
+
+__global__ __launch_bounds__(256) void k_ct_count(const int32_t *__restrict__ w_oc, const int16_t *__restrict__ w_ic,
+                                                  int64_t OC, int64_t IC, int32_t *__restrict__ t_ic_ptr) {
+    const int64_t ic = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ic >= IC) return;
+    int32_t n = 0;
+    for (int64_t oc = 0; oc < OC; ++oc) n += w_ic[oc * (IC + 1) + ic + 1] - w_ic[oc * (IC + 1) + ic];
+    t_ic_ptr[ic + 1] = n;
+}
+
+__global__ __launch_bounds__(256) void k_ct_fill(const int32_t *__restrict__ w_oc, const int16_t *__restrict__ w_ic,
+                                                 int64_t OC, int64_t IC, const int32_t *__restrict__ t_ic_ptr,
+                                                 int32_t *__restrict__ t_oc, int32_t *__restrict__ t_perm) {
+    const int64_t ic = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ic >= IC) return;
+    int32_t pos = t_ic_ptr[ic];
+    for (int64_t oc = 0; oc < OC; ++oc) {
+        const int32_t s0 = run_begin(w_oc, w_ic, IC, oc, ic), s1 = run_begin(w_oc, w_ic, IC, oc, ic + 1);
+        for (int32_t si = s0; si < s1; ++si) {
+            t_oc[pos] = (int32_t)oc;
+            t_perm[pos] = si;
+            ++pos;
+        }
+    }
+}
+
+sp_status transpose_build(int64_t OC, int64_t IC, const int32_t *w_oc, const int16_t *w_ic, int64_t nnz,
+                          int32_t *t_ic_ptr, int32_t *t_oc, int32_t *t_perm, hipStream_t st) {
+    sp_status s;
+    if ((s = sp::fill_i32(t_ic_ptr, IC + 1, 0, st))) return s;
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_ct_count, dim3((unsigned)sp::ceil_div(IC, 256)), dim3(256), 0, st, w_oc, w_ic, OC, IC,
+                           t_ic_ptr);
+        SP_CHECK_LAUNCH();
+    }
+    if ((s = sp::scan_counts(t_ic_ptr, IC, st))) return s;
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_ct_fill, dim3((unsigned)sp::ceil_div(IC, 256)), dim3(256), 0, st, w_oc, w_ic, OC, IC,
+                           t_ic_ptr, t_oc, t_perm);
+        SP_CHECK_LAUNCH();
+    }
+    return SP_OK;
+}
+
+// Column of every entry in the forward orientation (row = oc): ic*KK + x*KW + y.
+__global__ __launch_bounds__(256) void k_col_fwd(const int32_t *__restrict__ w_oc, const int16_t *__restrict__ w_ic,
+                                                 const uint8_t *__restrict__ w_x, const uint8_t *__restrict__ w_y,
+                                                 int64_t OC, int64_t IC, int KW, int KK, int32_t *__restrict__ col) {
+    const int lane = threadIdx.x & 63;
+    const int64_t oc = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (oc >= OC) return;
+    for (int64_t ic = lane; ic < IC; ic += 64) {
+        const int32_t s0 = run_begin(w_oc, w_ic, IC, oc, ic), s1 = run_begin(w_oc, w_ic, IC, oc, ic + 1);
+        for (int32_t si = s0; si < s1; ++si) col[si] = (int32_t)ic * KK + w_x[si] * KW + w_y[si];
+    }
+}
+
+// Column of every position of the input-channel-major view (row = ic): oc*KK + x*KW + y.
+__global__ __launch_bounds__(256) void k_col_bwd(const int32_t *__restrict__ t_oc, const int32_t *__restrict__ t_perm,
+                                                 const uint8_t *__restrict__ w_x, const uint8_t *__restrict__ w_y,
+                                                 int64_t nnz, int KW, int KK, int32_t *__restrict__ col) {
+    const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= nnz) return;
+    const int32_t si = t_perm[k];
+    col[k] = t_oc[k] * KK + w_x[si] * KW + w_y[si];
+}
+
+__global__ void k_zero(float *p, int64_t n) {
+    int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+    for (; i < n; i += stride) p[i] = 0.f;
+}
+
+sp_status zero_launch(float *p, int64_t n, hipStream_t st) {
+    if (n <= 0) return SP_OK;
+    hipLaunchKernelGGL(k_zero, dim3((unsigned)std::min<int64_t>(sp::ceil_div(n, 256), 4096)), dim3(256), 0, st, p, n);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+// --------------------------------------------------------------------------
+// Convolution geometry for the tiled kernels.
+//   DIR 0: gather X by output pixels (forward, weight gradient);
+//   DIR 1: gather dY by input pixels, unit stride (input gradient);
+//   DIR 2: gather dY by input pixels, any stride (input gradient).
+// Staging: thread tid holds token tid & 255 of the tile and the 16
+// consecutive columns 16*(tid >> 8) .. +15 of the slab, so a wave
+// instruction loads one column for 64 consecutive pixels and the column's
+// (channel, x, y) is wave-uniform.  Output and the stationary operand of the
+// weight gradient go through LDS (two halves of 128 tokens) so that global
+// accesses are runs of consecutive pixels of one channel.
+template <int DIR>
+struct ConvGeo {
+    const float *G;   // gathered tensor
+    int gbytes;       // its size in bytes (< 2 GiB)
+    int ntok;         // tokens = images * npix
+    int npix, tw;     // pixels per image of the token grid and its width
+    int ncols;        // channels of G * KH * KW
+    int KH, KW, KK;
+    int gH, gW, gplane, gimg;  // G: plane height/width, plane size, image size (elements)
+    int sh, sw, ph, pw;
+    float *Out;       // SpMM output [images][orows][npix]
+    const float *D;   // SDDMM stationary operand, same layout as Out
+    int orows;
+
+    struct Tok {
+        int a, c;      // spatial origin of the staging token (see tile_init)
+        int gbase;     // element offset of that origin in G
+        int obase[2];  // element offset of the output pixels (tid & 127) + 128h, -1 if past the end
+    };
+
+    __device__ void tile_init(Tok &tk, int64_t t0, int) const {
+        const int tid = threadIdx.x;
+        const int tg = (int)t0 + (tid & 255);
+        tk.a = TOK_INVALID;
+        tk.c = TOK_INVALID;
+        tk.gbase = 0;
+        if (tg < ntok) {
+            const int b = tg / npix, pix = tg - b * npix;
+            const int r = pix / tw, s = pix - r * tw;
+            if (DIR == 0) {
+                tk.a = r * sh - ph;
+                tk.c = s * sw - pw;
+                tk.gbase = b * gimg + tk.a * gW + tk.c;
+            } else {
+                tk.a = r + ph;
+                tk.c = s + pw;
+                tk.gbase = DIR == 1 ? b * gimg + tk.a * gW + tk.c : b * gimg;
+            }
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int ts = (int)t0 + (tid & 127) + 128 * h;
+            int ob = -1;
+            if (ts < ntok) {
+                const int b = ts / npix;
+                ob = b * orows * npix + (ts - b * npix);
+            }
+            tk.obase[h] = ob;
+        }
+    }
+
+    __device__ uint32_t load_slab(float (&pf)[PF], const Tok &tk, int64_t, int64_t c0, int tid) const {
+        static_assert(PF == 16, "conv staging assumes 16 columns per thread");
+        const sp_i32x4 rsrc = sp::make_rsrc(G, (uint32_t)gbytes);
+        const int cb = (int)c0 + 16 * __builtin_amdgcn_readfirstlane(tid >> 8);
+        int ch = cb / KK;
+        const int tap = cb - ch * KK;
+        int x = tap / KW;
+        int y = tap - x * KW;
+#pragma unroll
+        for (int i = 0; i < PF; ++i) {
+            const bool col_ok = cb + i < ncols;
+            bool ok;
+            int off;
+            if (DIR == 0) {
+                ok = (unsigned)(tk.a + x) < (unsigned)gH && (unsigned)(tk.c + y) < (unsigned)gW;
+                off = tk.gbase + ch * gplane + x * gW + y;
+            } else if (DIR == 1) {
+                ok = (unsigned)(tk.a - x) < (unsigned)gH && (unsigned)(tk.c - y) < (unsigned)gW;
+                off = tk.gbase + ch * gplane - x * gW - y;
+            } else {
+                const int dh = tk.a - x, dw = tk.c - y;
+                const unsigned qh = (unsigned)dh / (unsigned)sh, qw = (unsigned)dw / (unsigned)sw;
+                ok = dh >= 0 && dw >= 0 && (int)qh * sh == dh && (int)qw * sw == dw && qh < (unsigned)gH &&
+                     qw < (unsigned)gW;
+                off = tk.gbase + ch * gplane + (int)qh * gW + (int)qw;
+            }
+            pf[i] = sp_raw_buffer_load_f32(rsrc, (ok && col_ok) ? (int)((unsigned)off * 4u) : OOB, 0, 0);
+            if (++y == KW) {
+                y = 0;
+                if (++x == KH) {
+                    x = 0;
+                    ++ch;
+                }
+            }
+        }
+        return 0xffffffffu;
+    }
+
+    __device__ void write_slab(float *xs, const float (&pf)[PF], uint32_t, const Tok &, int tid) const {
+        float *x = xs + (tid >> 8) * 16 * TS + (tid & 255);
+#pragma unroll
+        for (int i = 0; i < PF; ++i) x[i * TS] = pf[i];
+    }
+
+    template <int RW>
+    __device__ void store(float *ys, const float (&acc)[RW][4], const Tok &tk, int64_t, int64_t row0, int tid,
+                          int lane, int rw0) const {
+        constexpr int R = NW * RW;
+        static_assert(R * YS <= spt::XS_FLOATS, "output staging exceeds the slab buffer");
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();
+            if ((lane >> 5) == h) {
+                const int tl = 4 * (lane & 31);
+#pragma unroll
+                for (int r = 0; r < RW; ++r)
+                    *reinterpret_cast<float4 *>(ys + (rw0 + r) * YS + tl) =
+                        make_float4(acc[r][0], acc[r][1], acc[r][2], acc[r][3]);
+            }
+            __syncthreads();
+            const int ob = tk.obase[h], tl = tid & 127;
+            if (ob >= 0) {
+                for (int r = tid >> 7; r < R; r += NTHR / 128) {
+                    const int64_t gr = row0 + r;
+                    if (gr < orows) Out[ob + gr * npix] = ys[r * YS + tl];
+                }
+            }
+        }
+    }
+
+    template <int RW>
+    __device__ void load_d(float *ys, float (&d)[RW][4], const Tok &tk, int64_t, int64_t row0, int tid, int lane,
+                           int rw0) const {
+        constexpr int R = NW * RW;
+        static_assert(R * YS <= spt::XS_FLOATS, "operand staging exceeds the slab buffer");
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            __syncthreads();
+            const int ob = tk.obase[h], tl = tid & 127;
+            for (int r = tid >> 7; r < R; r += NTHR / 128) {
+                const int64_t gr = row0 + r;
+                ys[r * YS + tl] = (ob >= 0 && gr < orows) ? D[ob + gr * npix] : 0.f;
+            }
+            __syncthreads();
+            if ((lane >> 5) == h) {
+                const int tl4 = 4 * (lane & 31);
+#pragma unroll
+                for (int r = 0; r < RW; ++r) {
+                    const float4 v = *reinterpret_cast<const float4 *>(ys + (rw0 + r) * YS + tl4);
+                    d[r][0] = v.x;
+                    d[r][1] = v.y;
+                    d[r][2] = v.z;
+                    d[r][3] = v.w;
+                }
+            }
+        }
+    }
+};
+
+// --------------------------------------------------------------------------
+// Shapes, plan layout, launches.
+
+struct Dims {
+    int64_t B, IC, H, W, OC, OH, OW;
+    int KH, KW, KK, sh, sw, ph, pw;
+};
+
+bool out_hw(const sp_conv_shape *s, int64_t *OH, int64_t *OW) {
+    if (!s || s->B < 0 || s->IC < 1 || s->OC < 1 || s->H < 1 || s->W < 1) return false;
+    if (s->KH < 1 || s->KW < 1 || s->KH > 255 || s->KW > 255) return false;
+    if (s->stride_h < 1 || s->stride_w < 1 || s->pad_h < 0 || s->pad_w < 0) return false;
+    const int64_t nh = s->H + 2 * (int64_t)s->pad_h - s->KH, nw = s->W + 2 * (int64_t)s->pad_w - s->KW;
+    if (nh < 0 || nw < 0) return false;
+    *OH = nh / s->stride_h + 1;
+    *OW = nw / s->stride_w + 1;
+    return true;
+}
+
+// Shape check shared by every entry point.  Returns SP_OK and fills d.
+sp_status dims_of(const sp_conv_shape *s, int64_t nnz, Dims &d) {
+    int64_t OH, OW;
+    if (!out_hw(s, &OH, &OW) || nnz < 0) return SP_ERR_INVALID_ARG;
+    d = Dims{s->B, s->IC, s->H, s->W, s->OC, OH, OW, s->KH, s->KW, s->KH * s->KW, s->stride_h, s->stride_w,
+             s->pad_h, s->pad_w};
+    if (d.IC * d.KK > 32767 || d.OC > 0x7fffffffLL / d.KK || nnz > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    if (nnz > d.OC * d.IC * d.KK) return SP_ERR_INVALID_ARG;
+    return SP_OK;
+}
+
+// Every activation tensor must span less than 2 GiB (buffer-load range).
+bool fits(const Dims &d) {
+    const double x = (double)d.B * (double)d.IC * (double)d.H * (double)d.W * 4.0;
+    const double y = (double)d.B * (double)d.OC * (double)d.OH * (double)d.OW * 4.0;
+    return x <= (double)MAX_BYTES && y <= (double)MAX_BYTES;
+}
+
+struct ConvPlan {
+    int32_t *t_ic_ptr, *t_oc, *t_perm;
+    int32_t *colA, *colB;
+    spt::Tiling A, Bt;  // A: rows = OC, columns (ic, tap); Bt: rows = IC, columns (oc, tap)
+    int32_t *cnt;
+    size_t bytes;
+};
+
+ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
+    sp::Carve c(const_cast<void *>(base));
+    ConvPlan L;
+    L.t_ic_ptr = c.take<int32_t>(d.IC + 1);
+    L.t_oc = c.take<int32_t>(nnz);
+    L.t_perm = c.take<int32_t>(nnz);
+    L.colA = c.take<int32_t>(nnz);
+    L.colB = c.take<int32_t>(nnz);
+    spt::tiling_layout(c, L.A, d.OC, d.IC * d.KK, nnz);
+    spt::tiling_layout(c, L.Bt, d.IC, d.OC * d.KK, nnz);
+    L.cnt = c.take<int32_t>(std::max(d.OC * L.A.K, d.IC * L.Bt.K));
+    L.bytes = c.off;
+    return L;
+}
+
+template <int DIR>
+ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
+    ConvGeo<DIR> g{};
+    g.KH = d.KH;
+    g.KW = d.KW;
+    g.KK = d.KK;
+    g.sh = d.sh;
+    g.sw = d.sw;
+    g.ph = d.ph;
+    g.pw = d.pw;
+    if (fwd_tokens) {  // tokens = output pixels, G = X, rows = OC
+        g.ntok = (int)(d.B * d.OH * d.OW);
+        g.npix = (int)(d.OH * d.OW);
+        g.tw = (int)d.OW;
+        g.ncols = (int)(d.IC * d.KK);
+        g.gH = (int)d.H;
+        g.gW = (int)d.W;
+        g.gplane = (int)(d.H * d.W);
+        g.gimg = (int)(d.IC * d.H * d.W);
+        g.gbytes = (int)(d.B * d.IC * d.H * d.W * 4);
+        g.orows = (int)d.OC;
+    } else {  // tokens = input pixels, G = dY, rows = IC
+        g.ntok = (int)(d.B * d.H * d.W);
+        g.npix = (int)(d.H * d.W);
+        g.tw = (int)d.W;
+        g.ncols = (int)(d.OC * d.KK);
+        g.gH = (int)d.OH;
+        g.gW = (int)d.OW;
+        g.gplane = (int)(d.OH * d.OW);
+        g.gimg = (int)(d.OC * d.OH * d.OW);
+        g.gbytes = (int)(d.B * d.OC * d.OH * d.OW * 4);
+        g.orows = (int)d.IC;
+    }
+    return g;
+}
+
+template <class Geo>
+sp_status spmm(const spt::Tiling &t, const Geo &geo, const float *vals, hipStream_t st) {
+    const int64_t ntiles = sp::ceil_div(geo.ntok, T);
+    const int64_t nwg = t.P * ntiles;
+    if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    if (nwg == 0) return SP_OK;
+    if (t.R == 128)
+        hipLaunchKernelGGL((spt::k_spmm<8, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
+                           (int)ntiles);
+    else
+        hipLaunchKernelGGL((spt::k_spmm<4, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
+                           (int)ntiles);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, T); }
+
+}  // namespace
+
+// ==========================================================================
+// C ABI
+
+extern "C" sp_status sp_conv_out_hw(const sp_conv_shape *s, int64_t *OH, int64_t *OW) {
+    if (!OH || !OW) return SP_ERR_INVALID_ARG;
+    return out_hw(s, OH, OW) ? SP_OK : SP_ERR_INVALID_ARG;
+}
+
+extern "C" sp_status sp_conv_encode_rows(int64_t OC, int64_t IC, int32_t KH, int32_t KW, const uint8_t *mask,
+                                         int32_t *w_oc, int16_t *w_ic, void *stream) {
+    if (OC < 1 || IC < 1 || KH < 1 || KW < 1 || !mask || !w_oc || !w_ic) return SP_ERR_INVALID_ARG;
+    if (KH > 255 || KW > 255 || IC * KH * KW > 32767) return SP_ERR_UNSUPPORTED;
+    hipStream_t st = (hipStream_t)stream;
+    hipLaunchKernelGGL(k_conv_encode_rows, dim3((unsigned)sp::ceil_div(OC, 4)), dim3(256), 0, st, mask, OC, IC,
+                       KH * KW, w_oc, w_ic);
+    SP_CHECK_LAUNCH();
+    return sp::scan_counts(w_oc, OC, st);
+}
+
+extern "C" sp_status sp_conv_encode_fill(int64_t OC, int64_t IC, int32_t KH, int32_t KW, const uint8_t *mask,
+                                         const float *W, const int32_t *w_oc, const int16_t *w_ic, uint8_t *w_x,
+                                         uint8_t *w_y, float *w_vals, void *stream) {
+    if (OC < 1 || IC < 1 || KH < 1 || KW < 1 || !mask || !W || !w_oc || !w_ic) return SP_ERR_INVALID_ARG;
+    if (KH > 255 || KW > 255 || IC * KH * KW > 32767) return SP_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(k_conv_encode_fill, dim3((unsigned)sp::ceil_div(OC, 4)), dim3(256), 0, (hipStream_t)stream,
+                       mask, W, OC, IC, KH, KW, w_oc, w_ic, w_x, w_y, w_vals);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+extern "C" sp_status sp_conv_transpose(int64_t OC, int64_t IC, const int32_t *w_oc, const int16_t *w_ic, int64_t nnz,
+                                       int32_t *t_ic_ptr, int32_t *t_oc, int32_t *t_perm, void *stream) {
+    if (OC < 1 || IC < 1 || nnz < 0 || nnz > 0x7fffffffLL || !w_oc || !w_ic || !t_ic_ptr) return SP_ERR_INVALID_ARG;
+    if (nnz > 0 && (!t_oc || !t_perm)) return SP_ERR_INVALID_ARG;
+    return transpose_build(OC, IC, w_oc, w_ic, nnz, t_ic_ptr, t_oc, t_perm, (hipStream_t)stream);
+}
+
+extern "C" sp_status sp_conv_plan_bytes(const sp_conv_shape *s, int64_t nnz, size_t *bytes) {
+    Dims d;
+    if (!bytes) return SP_ERR_INVALID_ARG;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    *bytes = plan_layout(nullptr, d, nnz).bytes;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_conv_plan(const sp_conv_shape *s, const int32_t *w_oc, const int16_t *w_ic, const uint8_t *w_x,
+                                  const uint8_t *w_y, int64_t nnz, void *plan, size_t plan_bytes, void *stream) {
+    Dims d;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    if (!w_oc || !w_ic || !plan || (nnz > 0 && (!w_x || !w_y))) return SP_ERR_INVALID_ARG;
+    ConvPlan L = plan_layout(plan, d, nnz);
+    if (plan_bytes < L.bytes) return SP_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    if ((r = transpose_build(d.OC, d.IC, w_oc, w_ic, nnz, L.t_ic_ptr, L.t_oc, L.t_perm, st))) return r;
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_col_fwd, dim3((unsigned)sp::ceil_div(d.OC, 4)), dim3(256), 0, st, w_oc, w_ic, w_x, w_y,
+                           d.OC, d.IC, d.KW, d.KK, L.colA);
+        SP_CHECK_LAUNCH();
+        hipLaunchKernelGGL(k_col_bwd, dim3((unsigned)sp::ceil_div(nnz, 256)), dim3(256), 0, st, L.t_oc, L.t_perm, w_x,
+                           w_y, nnz, d.KW, d.KK, L.colB);
+        SP_CHECK_LAUNCH();
+    }
+    if ((r = spt::tiling_build(L.A, w_oc, L.colA, nullptr, L.cnt, st))) return r;
+    return spt::tiling_build(L.Bt, L.t_ic_ptr, L.colB, L.t_perm, L.cnt, st);
+}
+
+extern "C" sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const float *w_vals, int64_t nnz,
+                                 const void *plan, float *Y, void *stream) {
+    Dims d;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    if (!plan || (d.B > 0 && (!X || !Y)) || (nnz > 0 && !w_vals)) return SP_ERR_INVALID_ARG;
+    if (!fits(d)) return SP_ERR_UNSUPPORTED;
+    if (d.B == 0) return SP_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (nnz == 0) return zero_launch(Y, d.B * d.OC * d.OH * d.OW, st);
+    ConvPlan L = plan_layout(plan, d, nnz);
+    ConvGeo<0> g = make_geo<0>(d, true);
+    g.G = X;
+    g.Out = Y;
+    return spmm(L.A, g, w_vals, st);
+}
+
+extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, const float *w_vals, int64_t nnz,
+                                       const void *plan, float *dX, void *stream) {
+    Dims d;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    if (!plan || (d.B > 0 && (!dY || !dX)) || (nnz > 0 && !w_vals)) return SP_ERR_INVALID_ARG;
+    if (!fits(d)) return SP_ERR_UNSUPPORTED;
+    if (d.B == 0) return SP_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (nnz == 0) return zero_launch(dX, d.B * d.IC * d.H * d.W, st);
+    ConvPlan L = plan_layout(plan, d, nnz);
+    if (d.sh == 1 && d.sw == 1) {
+        ConvGeo<1> g = make_geo<1>(d, false);
+        g.G = dY;
+        g.Out = dX;
+        return spmm(L.Bt, g, w_vals, st);
+    }
+    ConvGeo<2> g = make_geo<2>(d, false);
+    g.G = dY;
+    g.Out = dX;
+    return spmm(L.Bt, g, w_vals, st);
+}
+
+extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes) {
+    Dims d;
+    if (!bytes) return SP_ERR_INVALID_ARG;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    *bytes = (nnz > 0 && d.B > 0) ? sp::align256((size_t)wgrad_tiles(d) * (size_t)spt::padded_cap(nnz) * 4) : 0;
+    return SP_OK;
+}
+
+extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const sp_conv_shape *s, int64_t nnz,
+                                        const void *plan, float *dW, void *workspace, size_t ws_bytes, void *stream) {
+    Dims d;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    if (!plan || (nnz > 0 && !dW) || (d.B > 0 && nnz > 0 && (!dY || !X))) return SP_ERR_INVALID_ARG;
+    if (!fits(d)) return SP_ERR_UNSUPPORTED;
+    size_t need;
+    sp_conv_bwd_weight_ws(s, nnz, &need);
+    if (need > 0 && (!workspace || ws_bytes < need)) return SP_ERR_WORKSPACE;
+    if (nnz == 0) return SP_OK;
+    hipStream_t st = (hipStream_t)stream;
+    if (d.B == 0) return zero_launch(dW, nnz, st);
+    ConvPlan L = plan_layout(plan, d, nnz);
+    const int64_t ntiles = wgrad_tiles(d);
+    const int64_t nwg = L.A.P * ntiles;
+    if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    ConvGeo<0> g = make_geo<0>(d, true);
+    g.G = X;
+    g.D = dY;
+    float *part = (float *)workspace;
+    if (L.A.R == 128)
+        hipLaunchKernelGGL((spt::k_sddmm<8, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
+                           (int)ntiles, L.A.cap, part);
+    else
+        hipLaunchKernelGGL((spt::k_sddmm<4, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
+                           (int)ntiles, L.A.cap, part);
+    SP_CHECK_LAUNCH();
+    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, st);
+}
+
+extern "C" sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW, const int32_t *w_oc,
+                                      const int16_t *w_ic, const uint8_t *w_x, const uint8_t *w_y, int64_t nnz) {
+    if (OC < 1 || IC < 1 || KH < 1 || KW < 1 || KH > 255 || KW > 255 || nnz < 0 || !w_oc || !w_ic)
+        return SP_ERR_INVALID_ARG;
+    if (nnz > 0 && (!w_x || !w_y)) return SP_ERR_INVALID_ARG;
+    if (w_oc[0] != 0 || w_oc[OC] != nnz) return SP_ERR_INVALID_ARG;
+    for (int64_t oc = 0; oc < OC; ++oc) {
+        if (w_oc[oc + 1] < w_oc[oc]) return SP_ERR_INVALID_ARG;
+        const int16_t *wi = w_ic + oc * (IC + 1);
+        if (wi[0] != 0 || wi[IC] != w_oc[oc + 1] - w_oc[oc]) return SP_ERR_INVALID_ARG;
+        for (int64_t ic = 0; ic < IC; ++ic) {
+            if (wi[ic + 1] < wi[ic]) return SP_ERR_INVALID_ARG;
+            int prev = -1;
+            for (int64_t si = w_oc[oc] + wi[ic]; si < w_oc[oc] + wi[ic + 1]; ++si) {
+                if (w_x[si] >= KH || w_y[si] >= KW) return SP_ERR_INVALID_ARG;
+                const int tap = w_x[si] * KW + w_y[si];
+                if (tap <= prev) return SP_ERR_INVALID_ARG;
+                prev = tap;
+            }
+        }
+    }
+    return SP_OK;
+}

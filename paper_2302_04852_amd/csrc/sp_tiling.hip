@@ -66,6 +66,11 @@ __global__ void k_fill_u16(uint16_t *p, int64_t n, uint16_t v) {
     for (; i < n; i += stride) p[i] = v;
 }
 
+// Sum over the token tiles in a fixed three-level blocking (runs of 16, runs
+// of 16 run sums, then the 256-tile block sums): every partial passes
+// through at most 32 + ntiles/256 additions, which keeps the fp32 rounding
+// bound small relative to the sum of absolute terms even for the longest
+// reductions (hundreds of thousands of pixels per weight).
 __global__ __launch_bounds__(256) void k_sddmm_reduce(const float *__restrict__ part, int64_t ntiles, int64_t cap,
                                                       const int32_t *__restrict__ e_src, float *__restrict__ grad) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -73,7 +78,17 @@ __global__ __launch_bounds__(256) void k_sddmm_reduce(const float *__restrict__ 
     const int32_t s = e_src[e];
     if (s < 0) return;
     float acc = 0.f;
-    for (int64_t q = 0; q < ntiles; ++q) acc += part[q * cap + e];
+    for (int64_t q2 = 0; q2 < ntiles; q2 += 256) {
+        const int64_t e2 = q2 + 256 < ntiles ? q2 + 256 : ntiles;
+        float s2 = 0.f;
+        for (int64_t q1 = q2; q1 < e2; q1 += 16) {
+            const int64_t e1 = q1 + 16 < e2 ? q1 + 16 : e2;
+            float s1 = 0.f;
+            for (int64_t q = q1; q < e1; ++q) s1 += part[q * cap + e];
+            s2 += s1;
+        }
+        acc += s2;
+    }
     grad[s] = acc;
 }
 
