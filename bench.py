@@ -13,7 +13,7 @@ rarely), and its preparation time is reported separately.
 
 Prints ONE JSON line.  Extra fields: `roofline` (dominant kernel: algorithmic
 bytes / FLOPs per launch over its event-timed duration), `cpu_baseline` (the
-CPU oracle timed on a bounded token sample on the host), `ops` (per-op times).
+CPU oracle timed on the host over whole repeated steps, about 10 s), `ops` (per-op times).
 """
 from __future__ import annotations
 
@@ -41,9 +41,53 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-tokens", type=int, default=1024,
-                    help="token sample for the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle baseline (whole steps are repeated)")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run only a plain device-to-device copy of COPY_BYTES (counter calibration)")
     return ap.parse_args()
+
+
+COPY_BYTES = 1 << 30
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm_k_sddmm_ffn_pair_hbm_traffic.txt")
+KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_tiled.h", "sp_tiling.hip", "sp_linear.hip"]
+
+
+def kernel_source_hash():
+    """sha256 over the sources of the kernels the bench launches."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2302_04852_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from the committed counter summary, or
+    None when it is absent or was taken on different kernel sources."""
+    try:
+        lines = open(TRAFFIC_FILE).read().splitlines()
+    except OSError:
+        return None
+    for line in lines:
+        if line.startswith("TRAFFIC "):
+            rec = json.loads(line[len("TRAFFIC "):])
+            if rec.get("source_hash") == kernel_source_hash() and kernel in rec.get("bytes_per_launch", {}):
+                return rec["bytes_per_launch"][kernel]
+    return None
+
+
+def calibrate_copy():
+    """A plain copy of COPY_BYTES, 5 times: under rocprofv3 --pmc its
+    FETCH_SIZE / WRITE_SIZE per dispatch give the counters' scale."""
+    import torch
+    a = torch.ones(COPY_BYTES // 4, device="cuda")
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "launches": 5}), flush=True)
 
 
 def linear_alg_bytes(op, B, in_f, out_f, nnz):
@@ -80,17 +124,20 @@ class Layer:
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path "
-              "(data-parallel sharding is described in DESIGN.md); run with --gpus 1", file=sys.stderr)
+        print("bench.py measures one GPU only (the library has no multi-GPU path); run with --gpus 1",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
-    import paper_2302_04852_amd as sp
-    from synth import linear_layer, FFN_PAIR, seed_for
-
     if not torch.cuda.is_available():
         print("no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
+
+    import paper_2302_04852_amd as sp
+    from synth import linear_layer, FFN_PAIR, seed_for
 
     layers_np = []
     for li, (name, out_f, in_f, B, s) in enumerate(FFN_PAIR):
@@ -129,29 +176,27 @@ def main():
         step()
     torch.cuda.synchronize()
 
-    # Timed region: K whole steps between two events on the launch stream.
+    # Timed region: K whole steps between two events on the launch stream,
+    # with an event pair around every op inside it (per-op durations).
     stream = torch.cuda.current_stream()
     e0 = torch.cuda.Event(enable_timing=True)
     e1 = torch.cuda.Event(enable_timing=True)
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
+           for _ in range(args.steps)]
     torch.cuda.synchronize()
     e0.record(stream)
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        for (name, f, _, _), (a, b) in zip(ops, evs[k]):
+            a.record(stream)
+            f()
+            b.record(stream)
     e1.record(stream)
     torch.cuda.synchronize()
     total_ms = e0.elapsed_time(e1)
     ms_per_step = total_ms / args.steps
-
-    # Per-op durations: events around each op over the same number of steps.
     per_op = {name: 0.0 for name, _, _, _ in ops}
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
-    for _ in range(args.steps):
-        for (name, f, _, _), (a, b) in zip(ops, evs):
-            a.record(stream)
-            f()
-            b.record(stream)
-        torch.cuda.synchronize()
-        for (name, _, _, _), (a, b) in zip(ops, evs):
+    for k in range(args.steps):
+        for (name, _, _, _), (a, b) in zip(ops, evs[k]):
             per_op[name] += a.elapsed_time(b)
     op_rows = {}
     for name, _, L, kind in ops:
@@ -165,15 +210,17 @@ def main():
     # of equal algorithmic work per step); the SDDMM kernel serves bwd_weight.
     spmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k in ("fwd", "bwd_input")])
     sddmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k == "bwd_weight"])
-    if sddmm_ms >= spmm_ms:
-        dom, dom_ms, kind = "k_sddmm (+reduce)", sddmm_ms, "bwd_weight"
+    if 2 * sddmm_ms >= 4 * spmm_ms:
+        dom, dom_ms, kind = "k_sddmm+k_sddmm_reduce", sddmm_ms, "bwd_weight"
     else:
         dom, dom_ms, kind = "k_spmm", spmm_ms, "fwd"
     fl = 2.0 * L1.nnz * B
     by = linear_alg_bytes(kind, B, L1.in_f, L1.out_f, L1.nnz)
     achieved_tf = fl / (dom_ms * 1e-3) / 1e12
+    traffic = measured_traffic(dom)
     roof = {"kernel": dom, "bound": "alu", "achieved": round(achieved_tf, 3), "peak": round(VALU_FP32_PEAK_TFLOPS, 1),
-            "unit": "TFLOP/s", "frac": round(achieved_tf / VALU_FP32_PEAK_TFLOPS, 4), "traffic": None,
+            "unit": "TFLOP/s", "frac": round(achieved_tf / VALU_FP32_PEAK_TFLOPS, 4), "traffic": traffic,
+            "source_hash": kernel_source_hash(),
             "alg_bytes_per_launch": by, "flops_per_launch": fl, "ms_per_launch": round(float(dom_ms), 5),
             "hbm_achieved_GBps": round(by / (dom_ms * 1e-3) / 1e9, 1), "hbm_peak_GBps": HBM_PEAK_GBS,
             "hbm_frac": round(by / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
@@ -204,33 +251,37 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers_np, args.cpu_tokens)
+        out["cpu_baseline"] = cpu_baseline(layers_np, args.cpu_seconds)
     print(json.dumps(out), flush=True)
 
 
-def cpu_baseline(layers_np, ntok):
-    """The CPU oracle (as it stands) on the same step, restricted to the first
-    `ntok` tokens; reported in the same effective-GFLOP/s unit."""
+def cpu_baseline(layers_np, min_seconds):
+    """The CPU oracle (as it stands) on the same six-op step over all tokens,
+    repeated until at least `min_seconds` have passed; reported in the same
+    effective-GFLOP/s unit."""
     import oracle
-    t_total = 0.0
-    flops = 0.0
-    X = layers_np[0]["X"][:ntok]
-    dY2 = layers_np[1]["dY"][:ntok]
-    enc = [oracle.linear_encode(d["mask"], d["W"]) for d in layers_np]
-    t = time.perf_counter()
-    (rp1, ci1, v1), (rp2, ci2, v2) = enc
+    X = layers_np[0]["X"]
+    dY2 = layers_np[1]["dY"]
+    ntok = X.shape[0]
+    (rp1, ci1, v1), (rp2, ci2, v2) = [oracle.linear_encode(d["mask"], d["W"]) for d in layers_np]
     o1, i1 = layers_np[0]["mask"].shape
     o2, i2 = layers_np[1]["mask"].shape
-    Y1, _ = oracle.linear_fwd(X, rp1, ci1, v1, o1)
-    Y1f = Y1.astype(np.float32)
-    oracle.linear_fwd(Y1f, rp2, ci2, v2, o2)
-    dX2, _ = oracle.linear_bwd_input(dY2, rp2, ci2, v2, i2)
-    oracle.linear_bwd_weight(dY2, Y1f, rp2, ci2)
-    dX2f = dX2.astype(np.float32)
-    oracle.linear_bwd_input(dX2f, rp1, ci1, v1, i1)
-    oracle.linear_bwd_weight(dX2f, X, rp1, ci1)
-    t_total = time.perf_counter() - t
-    flops = 3 * 2.0 * (len(v1) + len(v2)) * ntok
+    reps = 0
+    t = time.perf_counter()
+    while True:
+        Y1, _ = oracle.linear_fwd(X, rp1, ci1, v1, o1)
+        Y1f = Y1.astype(np.float32)
+        oracle.linear_fwd(Y1f, rp2, ci2, v2, o2)
+        dX2, _ = oracle.linear_bwd_input(dY2, rp2, ci2, v2, i2)
+        oracle.linear_bwd_weight(dY2, Y1f, rp2, ci2)
+        dX2f = dX2.astype(np.float32)
+        oracle.linear_bwd_input(dX2f, rp1, ci1, v1, i1)
+        oracle.linear_bwd_weight(dX2f, X, rp1, ci1)
+        reps += 1
+        t_total = time.perf_counter() - t
+        if t_total >= min_seconds:
+            break
+    flops = reps * 3 * 2.0 * (len(v1) + len(v2)) * ntok
     cpu_model = ""
     try:
         for line in open("/proc/cpuinfo"):
@@ -241,8 +292,9 @@ def cpu_baseline(layers_np, ntok):
         pass
     return {"value": round(flops / t_total / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
             "kind": "oracle", "seconds": round(t_total, 2), "cpu": cpu_model,
-            "sample": "same six-op FFN step on the first %d of 8192 tokens (fp64-accumulating plain loops, "
-                      "OpenMP over independent outputs)" % ntok}
+            "sample": "the same six-op FFN step over all %d tokens, repeated %d times (fp64-accumulating "
+                      "plain loops, OpenMP over independent outputs; conversions between ops included)"
+                      % (ntok, reps)}
 
 
 if __name__ == "__main__":
