@@ -4,6 +4,7 @@
 // weight gradient sampled at the stored entries (Eq. 2).  The compute work
 // runs in the tiled kernels of sp_tiled.h; this file supplies the linear
 // geometry: tokens are rows of row-major [B][features] matrices.
+#include "sp_spmm2.h"
 #include "sp_tiled.h"
 
 namespace {
@@ -275,11 +276,122 @@ struct LinGeo {
     }
 };
 
+// Linear geometry of the row-slot SpMM (sp_spmm2.h).  G is In[ntok][ld]
+// (columns < ncols), the output Out[ntok][ldo] (rows < nrows).  Staging:
+// thread tid holds tokens 4*(tid & 15) .. +3 and, in each part h of the
+// chunk, columns CW*h + 4*(tid >> 4) .. +3 (CW = 4 * threads / 16) -- 16-byte
+// loads of four token rows, written to LDS as 16-byte columns.  MODE as for
+// LinGeo.
+template <int MODE>
+struct LinGeo2 {
+    const float *In;
+    int64_t ntok, ld, ncols;
+    float *Out;
+    int64_t ldo, nrows;
+    static constexpr int CW = 4 * (spt2::NTHR / 16);  // chunk columns covered by one part
+    static constexpr int NH = spt2::KC / CW;          // parts per chunk
+
+    struct Tok {
+        sp_i32x4 rsrc;
+        int voff;  // byte offset of (token row 4*tq, column 4*cq) within the tile (MODE 2)
+        int64_t t0;
+    };
+    __device__ void tile_init(Tok &tk, int64_t t0) const {
+        const int tq = threadIdx.x & 15, cq = threadIdx.x >> 4;
+        tk.t0 = t0;
+        if (MODE == 2) {
+            tk.rsrc = sp::make_rsrc(In + t0 * ld, (uint32_t)((ntok - t0) * ld * 4));
+            tk.voff = (int)((4 * tq * ld + 4 * cq) * 4);
+        }
+    }
+    __device__ uint32_t load_chunk(float (&pf)[spt2::PF], const Tok &tk, int64_t c0) const {
+        const int tq = threadIdx.x & 15, cq = threadIdx.x >> 4;
+        uint32_t mask = 0;
+#pragma unroll
+        for (int hh = 0; hh < NH; ++hh) {
+            const int64_t gc = c0 + CW * hh + 4 * cq;
+            if (MODE == 2) {
+                const bool ok = gc < ncols;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int vo = ok ? tk.voff + (int)(i * ld * 4 + (c0 + CW * hh) * 4) : 0x7ffffff0;
+                    const sp_f32x4 v = sp_raw_buffer_load_f32x4(tk.rsrc, vo, 0, 0);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) pf[16 * hh + 4 * i + e] = v[e];
+                }
+                continue;
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const int64_t gt = tk.t0 + 4 * tq + i;
+                const int64_t ct = gt < ntok ? gt : ntok - 1;
+                if (MODE == 1) {
+                    const int64_t cc = gc < ncols ? gc : ncols - 4;
+                    const float4 v = *reinterpret_cast<const float4 *>(In + ct * ld + cc);
+                    pf[16 * hh + 4 * i + 0] = v.x;
+                    pf[16 * hh + 4 * i + 1] = v.y;
+                    pf[16 * hh + 4 * i + 2] = v.z;
+                    pf[16 * hh + 4 * i + 3] = v.w;
+                    if (gt < ntok && gc < ncols) mask |= 0xfu << (16 * hh + 4 * i);
+                } else {
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int64_t ge = gc + e;
+                        pf[16 * hh + 4 * i + e] = In[ct * ld + (ge < ncols ? ge : ncols - 1)];
+                        if (gt < ntok && ge < ncols) mask |= 1u << (16 * hh + 4 * i + e);
+                    }
+                }
+            }
+        }
+        return MODE == 2 ? 0xffffffffu : mask;
+    }
+    __device__ void write_chunk(float *xs, const float (&pf)[spt2::PF], uint32_t mask, const Tok &) const {
+        const int tq = threadIdx.x & 15, cq = threadIdx.x >> 4;
+        float4 *x4 = reinterpret_cast<float4 *>(xs);
+#pragma unroll
+        for (int hh = 0; hh < NH; ++hh)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                float v[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int b = 16 * hh + 4 * i + j;
+                    v[i] = (MODE == 2 || ((mask >> b) & 1u)) ? pf[b] : 0.f;
+                }
+                x4[(CW * hh + 4 * cq + j) * (spt2::T / 4) + tq] = make_float4(v[0], v[1], v[2], v[3]);
+            }
+    }
+    // Accumulators -> Out through LDS: ys[position][token], then each thread
+    // writes one row position for a stride of tokens (row segments coalesce).
+    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &, int64_t t0, int64_t row0) const {
+        const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
+        __syncthreads();
+#pragma unroll
+        for (int s = 0; s < spt2::NS; ++s) {
+            const int pos = spt2::NG * spt2::NW * s + spt2::NG * w + g;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) ys[pos * spt2::YS + 4 * gl + k] = acc[s][k];
+        }
+        __syncthreads();
+        constexpr int TSTEP = spt2::NTHR / spt2::R;
+        const int rl = tid % spt2::R;
+        const int64_t row = row0 + rl;
+        if (row < nrows) {
+#pragma unroll 4
+            for (int t = tid / spt2::R; t < spt2::T; t += TSTEP) {
+                const int64_t gt = t0 + t;
+                if (gt < ntok) Out[gt * ldo + row] = ys[rl * spt2::YS + t];
+            }
+        }
+    }
+};
+
 // Plan layout: a pure function of (in_f, out_f, nnz).
 struct PlanLayout {
     int32_t *t_col_ptr, *t_row_idx, *t_perm;
-    spt::Tiling A, Bt;  // A: rows = out_f (forward, weight gradient); Bt: rows = in_f (input gradient)
-    int32_t *cnt;       // scratch [max(out_f*KA, in_f*KB)]
+    spt::Tiling A;         // rows = out_f: weight gradient
+    spt2::SlotTiling F, G; // row slots: F rows = out_f (forward), G rows = in_f (input gradient)
+    int32_t *cnt;          // scratch [max over the tilings of rows * chunks]
     int32_t *blk_cnt;   // transpose scratch [ceil(out_f/TR_BLK) * in_f]
     size_t bytes;
 };
@@ -291,8 +403,9 @@ PlanLayout plan_layout(const void *base, int64_t in_f, int64_t out_f, int64_t nn
     L.t_row_idx = c.take<int32_t>(nnz);
     L.t_perm = c.take<int32_t>(nnz);
     spt::tiling_layout(c, L.A, out_f, in_f, nnz);
-    spt::tiling_layout(c, L.Bt, in_f, out_f, nnz);
-    L.cnt = c.take<int32_t>(std::max(out_f * L.A.K, in_f * L.Bt.K));
+    spt2::slot_layout(c, L.F, out_f, in_f, nnz);
+    spt2::slot_layout(c, L.G, in_f, out_f, nnz);
+    L.cnt = c.take<int32_t>(std::max(out_f * L.A.K, std::max(out_f * L.F.K, in_f * L.G.K)));
     L.blk_cnt = c.take<int32_t>(sp::ceil_div(out_f, TR_BLK) * in_f);
     L.bytes = c.off;
     return L;
@@ -313,16 +426,12 @@ int lin_mode(int64_t ntok, int64_t ncols) {
 }
 
 template <int MODE>
-sp_status spmm_launch_t(const spt::Tiling &t, const LinGeo<MODE> &geo, const float *vals, hipStream_t st) {
-    const int64_t ntiles = ntiles_of(geo.ntok);
+sp_status spmm_launch_t(const spt2::SlotTiling &t, const LinGeo2<MODE> &geo, const float *vals, hipStream_t st) {
+    const int64_t ntiles = sp::ceil_div(geo.ntok, spt2::T);
     const int64_t nwg = t.P * ntiles;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
-    if (t.R == 128)
-        hipLaunchKernelGGL((spt::k_spmm<8, LinGeo<MODE>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals,
-                           t.view(), (int)ntiles);
-    else
-        hipLaunchKernelGGL((spt::k_spmm<4, LinGeo<MODE>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals,
-                           t.view(), (int)ntiles);
+    hipLaunchKernelGGL((spt2::k_spmm2<LinGeo2<MODE>>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals,
+                       t.view(), (int)ntiles);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
@@ -330,7 +439,7 @@ sp_status spmm_launch_t(const spt::Tiling &t, const LinGeo<MODE> &geo, const flo
 __global__ void k_zero_f32(float *p, int64_t n);
 
 // Out[ntok][nrows] = sparse product over tiling t of In[ntok][ncols].
-sp_status spmm_launch(const spt::Tiling &t, const float *In, int64_t ntok, int64_t ncols, float *Out,
+sp_status spmm_launch(const spt2::SlotTiling &t, const float *In, int64_t ntok, int64_t ncols, float *Out,
                       int64_t nrows, const float *vals, int64_t nnz, hipStream_t st) {
     if (ntok == 0 || nrows == 0) return SP_OK;
     if (nnz == 0) {  // no stored entries: the product is zero
@@ -341,10 +450,10 @@ sp_status spmm_launch(const spt::Tiling &t, const float *In, int64_t ntok, int64
     }
     const int mode = lin_mode(ntok, ncols);
     if (mode == 2)
-        return spmm_launch_t<2>(t, LinGeo<2>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+        return spmm_launch_t<2>(t, LinGeo2<2>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
     if (mode == 1)
-        return spmm_launch_t<1>(t, LinGeo<1>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
-    return spmm_launch_t<0>(t, LinGeo<0>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+        return spmm_launch_t<1>(t, LinGeo2<1>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
+    return spmm_launch_t<0>(t, LinGeo2<0>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
 }
 
 __global__ void k_zero_f32(float *p, int64_t n) {  // definition
@@ -419,7 +528,8 @@ extern "C" sp_status sp_linear_plan(int64_t in_f, int64_t out_f, const int32_t *
     if ((s = csc_build(in_f, out_f, row_ptr, col_idx, nnz, L.t_col_ptr, L.t_row_idx, L.t_perm, L.blk_cnt, st)))
         return s;
     if ((s = spt::tiling_build(L.A, row_ptr, col_idx, nullptr, L.cnt, st))) return s;
-    return spt::tiling_build(L.Bt, L.t_col_ptr, L.t_row_idx, L.t_perm, L.cnt, st);
+    if ((s = spt2::slot_build(L.F, row_ptr, col_idx, nullptr, L.cnt, st))) return s;
+    return spt2::slot_build(L.G, L.t_col_ptr, L.t_row_idx, L.t_perm, L.cnt, st);
 }
 
 extern "C" sp_status sp_linear_plan_csc(const void *plan, int64_t in_f, int64_t out_f, int64_t nnz,
@@ -443,7 +553,7 @@ extern "C" sp_status sp_linear_fwd(const float *X, int64_t B, int64_t in_f, int6
     if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
     if ((B * out_f > 0 && !Y) || (B * in_f > 0 && !X) || (nnz > 0 && !vals)) return SP_ERR_INVALID_ARG;
     PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
-    return spmm_launch(L.A, X, B, in_f, Y, out_f, vals, nnz, (hipStream_t)stream);
+    return spmm_launch(L.F, X, B, in_f, Y, out_f, vals, nnz, (hipStream_t)stream);
 }
 
 extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f, const float *vals,
@@ -451,7 +561,7 @@ extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_
     if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
     if ((B * in_f > 0 && !dX) || (B * out_f > 0 && !dY) || (nnz > 0 && !vals)) return SP_ERR_INVALID_ARG;
     PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
-    return spmm_launch(L.Bt, dY, B, out_f, dX, in_f, vals, nnz, (hipStream_t)stream);
+    return spmm_launch(L.G, dY, B, out_f, dX, in_f, vals, nnz, (hipStream_t)stream);
 }
 
 extern "C" sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f, int64_t nnz, size_t *bytes) {
