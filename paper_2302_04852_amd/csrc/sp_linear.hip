@@ -288,6 +288,8 @@ struct LinGeo2 {
     int64_t ntok, ld, ncols;
     float *Out;
     int64_t ldo, nrows;
+    const float *D;  // SDDMM stationary operand D[ntok][ldd] (rows < nrows)
+    int64_t ldd;
     static constexpr int CW = 4 * (spt2::NTHR / 16);  // chunk columns covered by one part
     static constexpr int NH = spt2::KC / CW;          // parts per chunk
 
@@ -360,6 +362,28 @@ struct LinGeo2 {
                 }
                 x4[(CW * hh + 4 * cq + j) * (spt2::T / 4) + tq] = make_float4(v[0], v[1], v[2], v[3]);
             }
+    }
+    // D[t0 + lane][row0 + 32*s + 4*w + 0..3]: the four rows of slot s (one per
+    // group of this wave) for this lane's token; zero past the last token or
+    // row.  With MODE 2 (and D 16-byte aligned per row) one 16-byte load.
+    __device__ float4 load_dq(const Tok &, int64_t t0, int64_t row0, int s) const {
+        const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+        const int64_t r = row0 + spt2::NG * spt2::NW * s + spt2::NG * w;
+        const int64_t t = t0 + lane;
+        const bool tok_ok = t < ntok;
+        const int64_t tc = tok_ok ? t : 0;
+        if (MODE == 2) {  // nrows % 4 == 0 and ldd == nrows: the four rows are all in range or all out
+            const float4 v = *reinterpret_cast<const float4 *>(D + tc * ldd + (r < nrows ? r : 0));
+            return (tok_ok && r < nrows) ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        float v[4];
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            const bool ok = tok_ok && r + g < nrows;
+            const float u = D[tc * ldd + (ok ? r + g : 0)];
+            v[g] = ok ? u : 0.f;
+        }
+        return make_float4(v[0], v[1], v[2], v[3]);
     }
     // Accumulators -> Out through LDS: ys[position][token], then each thread
     // writes one row position for a stride of tokens (row segments coalesce).
@@ -450,10 +474,10 @@ sp_status spmm_launch(const spt2::SlotTiling &t, const float *In, int64_t ntok, 
     }
     const int mode = lin_mode(ntok, ncols);
     if (mode == 2)
-        return spmm_launch_t<2>(t, LinGeo2<2>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
+        return spmm_launch_t<2>(t, LinGeo2<2>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
     if (mode == 1)
-        return spmm_launch_t<1>(t, LinGeo2<1>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
-    return spmm_launch_t<0>(t, LinGeo2<0>{In, ntok, ncols, ncols, Out, nrows, nrows}, vals, st);
+        return spmm_launch_t<1>(t, LinGeo2<1>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
+    return spmm_launch_t<0>(t, LinGeo2<0>{In, ntok, ncols, ncols, Out, nrows, nrows, nullptr, 0}, vals, st);
 }
 
 __global__ void k_zero_f32(float *p, int64_t n) {  // definition
@@ -566,7 +590,13 @@ extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_
 
 extern "C" sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f, int64_t nnz, size_t *bytes) {
     if (!bytes || B < 0 || bad_dims(in_f, out_f, nnz)) return SP_ERR_INVALID_ARG;
-    *bytes = nnz > 0 ? sp::align256((size_t)ntiles_of(B) * (size_t)spt::padded_cap(nnz) * 4) : 0;
+    if (nnz == 0 || B == 0) {
+        *bytes = 0;
+        return SP_OK;
+    }
+    const PlanLayout L = plan_layout(nullptr, in_f, out_f, nnz);
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, sp::ceil_div(B, spt2::T));
+    *bytes = sp::align256((size_t)sp2.nsplit * (size_t)spt2::part_stride(L.F) * 4);
     return SP_OK;
 }
 
@@ -588,28 +618,26 @@ extern "C" sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64
         return SP_OK;
     }
     PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
-    const int64_t ntiles = ntiles_of(B);
-    const int64_t nwg = L.A.P * ntiles;
+    const int64_t ntiles = sp::ceil_div(B, spt2::T);
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, ntiles);
+    const int64_t nwg = L.F.P * L.F.K * sp2.nsplit;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     float *part = (float *)workspace;
+    const int64_t pstride = spt2::part_stride(L.F);
     auto launch = [&](auto geo) {
         using G = decltype(geo);
-        if (L.A.R == 128)
-            hipLaunchKernelGGL((spt::k_sddmm<8, G>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, L.A.view(),
-                               (int)ntiles, L.A.cap, part);
-        else
-            hipLaunchKernelGGL((spt::k_sddmm<4, G>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, L.A.view(),
-                               (int)ntiles, L.A.cap, part);
+        hipLaunchKernelGGL((spt2::k_sddmm2<G>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, L.F.view(),
+                           (int)ntiles, sp2.nsplit, sp2.tps, part, pstride);
     };
-    const int mode = lin_mode(B, in_f);
+    const int mode = (lin_mode(B, in_f) == 2 && out_f % 4 == 0) ? 2 : std::min(lin_mode(B, in_f), 1);
     if (mode == 2)
-        launch(LinGeo<2>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+        launch(LinGeo2<2>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
     else if (mode == 1)
-        launch(LinGeo<1>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+        launch(LinGeo2<1>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
     else
-        launch(LinGeo<0>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+        launch(LinGeo2<0>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
     SP_CHECK_LAUNCH();
-    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, st);
+    return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
 }
 
 extern "C" sp_status sp_linear_validate(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,

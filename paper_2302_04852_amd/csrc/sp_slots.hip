@@ -98,9 +98,30 @@ __global__ __launch_bounds__(256) void k_slot_fill(const int32_t *__restrict__ p
     }
 }
 
+__global__ __launch_bounds__(256) void k_slot_reduce(const int2 *__restrict__ meta, int64_t npos,
+                                                     const float *__restrict__ part, int nsplit, int64_t pstride,
+                                                     float *__restrict__ grad) {
+    const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (pos >= npos) return;
+    const int32_t e = meta[pos].y;
+    if (e < 0) return;
+    float acc = 0.f;
+    for (int j = 0; j < nsplit; ++j) acc += part[(int64_t)j * pstride + pos];
+    grad[e] = acc;
+}
+
 }  // namespace
 
 namespace spt2 {
+
+sp_status slot_reduce(const SlotTiling &t, const float *part, int nsplit, int64_t pstride, float *grad,
+                      hipStream_t st) {
+    const int64_t npos = (t.nblk_cap + 1) * BLK;
+    hipLaunchKernelGGL(k_slot_reduce, dim3((unsigned)sp::ceil_div(npos, 256)), dim3(256), 0, st, t.meta, npos, part,
+                       nsplit, pstride, grad);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
 
 sp_status slot_build(const SlotTiling &t, const int32_t *ptr, const int32_t *idx, const int32_t *src_map,
                      int32_t *cnt, hipStream_t st) {

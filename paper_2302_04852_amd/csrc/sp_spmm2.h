@@ -1,7 +1,9 @@
-// Sparse x dense product with row slots held in registers (forward and input
-// gradient of both layer types).
+// Sparse kernels with row slots held in registers: the sparse x dense product
+// (forward and input gradient of both layer types) and the sampled dense x
+// dense product (weight gradient).
 //
-//   Out[t][r] = sum over the stored entries e of row r of val(e) * G[t][col(e)]
+//   SpMM   Out[t][r] = sum over the stored entries e of row r of val(e) * G[t][col(e)]
+//   SDDMM  grad(e)   = sum over tokens t of D[t][row(e)] * G[t][col(e)]
 //
 // Work decomposition.  A workgroup of 8 waves computes a tile of 64 tokens x
 // 256 rows.  A wave is 4 groups of 16 lanes; each lane owns 4 consecutive
@@ -218,5 +220,233 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
     }
     geo.store(xs, acc, tok, t0, (int64_t)p * R);
 }
+
+
+// --------------------------------------------------------------------------
+// SDDMM over the same slot tiling.  A workgroup takes one (panel, chunk) and a
+// contiguous range of token tiles (a split).  Per token tile, each lane loads
+// D for its 4 tokens and its 8 slot rows into registers and the chunk of G
+// is staged as for the SpMM.  For one metadata block, every lane forms the
+// 4-token partial product of each of the 16 iterations; a transpose-reduce
+// across the 16 lanes of the group (four DPP exchange stages) leaves in lane
+// i of group g the 64-token sum of entry (i, g) -- the entry whose metadata
+// that lane holds -- so one register per block accumulates over the token
+// tiles of the split.  At the end every lane writes its entries' sums to
+// part[split][block*64 + lane position]; a second kernel adds the splits in a
+// fixed order.  Slots with more than JMAX blocks in the chunk are handled in
+// further rounds over the token range.
+constexpr int JMAX = 2;
+
+template <int C>
+__device__ inline float dpp_mov(float v) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), C, 0xf, 0xf, true));
+}
+
+// Lane l (of a 16-lane row) receives the sum over the row's lanes of p[l].
+// Stage m pairs index i with i^m: lanes with bit m clear keep index i and add
+// the partner lane l+m (row_shl:m), lanes with bit m set keep i|m and add
+// lane l-m (row_shr:m).
+// LDS reads of iterations I and I+1 of a block (I a compile-time constant after unrolling).
+__device__ inline void ld2(float4 &x0, float4 &x1, int I, int off, const char *xb) {
+    switch (I) {
+#define SP2_LD2(K) case K: x0 = *reinterpret_cast<const float4 *>(xb + bcast16<K>(off)); \
+                          x1 = *reinterpret_cast<const float4 *>(xb + bcast16<K + 1>(off)); break;
+        SP2_LD2(0) SP2_LD2(2) SP2_LD2(4) SP2_LD2(6) SP2_LD2(8) SP2_LD2(10) SP2_LD2(12)
+        default: x0 = *reinterpret_cast<const float4 *>(xb + bcast16<14>(off));
+                 x1 = *reinterpret_cast<const float4 *>(xb + bcast16<15>(off)); break;
+#undef SP2_LD2
+    }
+}
+
+template <int M, int N>
+__device__ inline void bfly_stage(float (&v)[2 * N], float (&o)[N], int gl) {
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        const float a = v[i] + dpp_mov<0x100 + M>(v[i]);
+        const float b = v[i + N] + dpp_mov<0x110 + M>(v[i + N]);
+        o[i] = (gl & M) ? b : a;
+    }
+}
+
+// Stage 8 of the transpose-reduce for one pair of iterations (i, i+8).
+__device__ inline float bfly8(float lo, float hi, int gl) {
+    const float a = lo + dpp_mov<0x108>(lo);
+    const float b = hi + dpp_mov<0x118>(hi);
+    return (gl & 8) ? b : a;
+}
+
+// Stages 4, 2, 1 of the transpose-reduce.
+__device__ inline float transpose_reduce8(float (&a)[8]) {
+    const int gl = threadIdx.x & 15;
+    float b[4], c[2], e[1];
+    bfly_stage<4, 4>(a, b, gl);
+    bfly_stage<2, 2>(b, c, gl);
+    bfly_stage<1, 1>(c, e, gl);
+    return e[0];
+}
+
+__device__ inline float dot4(const float (&d)[4], const float4 &x) {
+    float v = d[0] * x.x;
+    v = fmaf(d[1], x.y, v);
+    v = fmaf(d[2], x.z, v);
+    return fmaf(d[3], x.w, v);
+}
+
+// Geometry addition for the SDDMM:
+//   float4 load_dq(tok, t0, row0, s)   D[t0 + lane][rows of slot s of groups 0..3 of this wave]
+template <class Geo>
+__global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_sddmm2(Geo geo, SlotView tv, int ntiles, int nsplit, int tps,
+                                                 float *__restrict__ part, int64_t pstride) {
+    __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
+    __shared__ __attribute__((aligned(16))) float dsx[NW * NG * T];  // per-wave D transpose scratch
+    __shared__ int rounds_s[NW];
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int P = tv.P, K = tv.K;
+    const int L = sp::xcd_remap(blockIdx.x, P * K * nsplit);
+    const int p = L % P, k = (L / P) % K, j = L / (P * K);
+    const int q0 = j * tps, q1 = min(ntiles, q0 + tps);
+    const int lp = 4 * (lane & 15) + (lane >> 4);
+    const char *xb = reinterpret_cast<const char *>(xs) + (lane & 15) * 16;
+    const int64_t row0 = (int64_t)p * R;
+
+    const int32_t *h = tv.hdr + (((int64_t)p * K + k) * NW + w) * HDR;
+    const int b0 = h[0];
+    int nb[NS], bs[NS], ms[NS];
+    int myr = 0, run = b0;
+#pragma unroll
+    for (int i = 0; i < NS / 2; ++i) {
+        const uint32_t v = (uint32_t)h[1 + i];
+        ms[2 * i] = (int)(v & 0xffffu);
+        ms[2 * i + 1] = (int)(v >> 16);
+    }
+#pragma unroll
+    for (int i = 0; i < NS; ++i) nb[i] = (ms[i] + 15) / 16;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        bs[s] = run;
+        run += nb[s];
+        myr = max(myr, (nb[s] + JMAX - 1) / JMAX);
+    }
+    if (lane == 0) rounds_s[w] = myr;
+    for (int i = tid; i < T; i += NTHR) xs[KC * T + i] = 0.f;
+    __syncthreads();
+    int rounds = 0;
+#pragma unroll
+    for (int i = 0; i < NW; ++i) rounds = max(rounds, rounds_s[i]);
+
+    for (int rho = 0; rho < rounds; ++rho) {
+        float acc[NS][JMAX];
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int jj = 0; jj < JMAX; ++jj) acc[s][jj] = 0.f;
+        for (int q = q0; q < q1; ++q) {
+            const int64_t t0 = (int64_t)q * T;
+            typename Geo::Tok tok;
+            geo.tile_init(tok, t0);
+            {
+                float pf[PF];
+                const uint32_t pfm = geo.load_chunk(pf, tok, (int64_t)k * KC);
+                __syncthreads();
+                geo.write_chunk(xs, pf, pfm, tok);
+            }
+            __syncthreads();
+            // D of one slot at a time: lane l loads token t0+l for the four rows
+            // of the slot (one per group), the next slot's load in flight; a
+            // per-wave LDS transpose hands lane (g, i) tokens 4i..4i+3 of row g.
+            // LDS operations of one wave execute in order, so the read sees
+            // the writes and the next slot's writes follow this read.  The
+            // column offsets of the slot's blocks are likewise loaded one slot
+            // ahead (blocks past the slot's count read padding metadata).
+            float *sc = dsx + w * (NG * T);
+            float4 dqn = geo.load_dq(tok, t0, row0, 0);
+            int offn[JMAX];
+#pragma unroll
+            for (int jj = 0; jj < JMAX; ++jj) offn[jj] = tv.meta[(int64_t)(bs[0] + rho * JMAX + jj) * BLK + lp].x;
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+                // keep each slot's loads where they are: hoisting all slots'
+                // prefetches to the top of the unrolled loop costs registers
+                __builtin_amdgcn_sched_barrier(0);
+                const float4 dq = dqn;
+                int off[JMAX];
+#pragma unroll
+                for (int jj = 0; jj < JMAX; ++jj) off[jj] = offn[jj];
+                if (s + 1 < NS) {
+                    dqn = geo.load_dq(tok, t0, row0, s + 1);
+#pragma unroll
+                    for (int jj = 0; jj < JMAX; ++jj)
+                        offn[jj] = tv.meta[(int64_t)(bs[s + 1] + rho * JMAX + jj) * BLK + lp].x;
+                }
+                sc[0 * T + lane] = dq.x;
+                sc[1 * T + lane] = dq.y;
+                sc[2 * T + lane] = dq.z;
+                sc[3 * T + lane] = dq.w;
+                __builtin_amdgcn_wave_barrier();
+                const float4 dv = *reinterpret_cast<const float4 *>(sc + (lane >> 4) * T + 4 * (lane & 15));
+                __builtin_amdgcn_wave_barrier();
+                const float d[4] = {dv.x, dv.y, dv.z, dv.w};
+#pragma unroll
+                for (int jj = 0; jj < JMAX; ++jj) {
+                    const int jb = rho * JMAX + jj;
+                    if (jb < nb[s]) {
+                        // iterations i and i+8 together: stage 8 of the reduce folds
+                        // them at once; the upper half is skipped when the block
+                        // holds at most 8 iterations
+                        const bool hi = ms[s] - 16 * jb > 8;
+                        const int gl = lane & 15;
+                        float av[8];
+                        if (hi) {
+#pragma unroll
+                            for (int i2 = 0; i2 < 8; i2 += 2) {
+                                float4 x0, x1, y0, y1;
+                                ld2(x0, x1, i2, off[jj], xb);
+                                ld2(y0, y1, i2 + 8, off[jj], xb);
+                                av[i2] = bfly8(dot4(d, x0), dot4(d, y0), gl);
+                                av[i2 + 1] = bfly8(dot4(d, x1), dot4(d, y1), gl);
+                            }
+                        } else {
+#pragma unroll
+                            for (int i2 = 0; i2 < 8; i2 += 2) {
+                                float4 x0, x1;
+                                ld2(x0, x1, i2, off[jj], xb);
+                                av[i2] = bfly8(dot4(d, x0), 0.f, gl);
+                                av[i2 + 1] = bfly8(dot4(d, x1), 0.f, gl);
+                            }
+                        }
+                        acc[s][jj] += transpose_reduce8(av);
+                    }
+                }
+            }
+        }
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int jj = 0; jj < JMAX; ++jj) {
+                const int jb = rho * JMAX + jj;
+                if (jb < nb[s]) part[(int64_t)j * pstride + (int64_t)(bs[s] + jb) * BLK + lp] = acc[s][jj];
+            }
+    }
+}
+
+// Token splits of the SDDMM grid: enough workgroups to give every compute
+// unit two of them, each split a contiguous range of tps >= 1 token tiles.
+struct Split {
+    int nsplit, tps;
+};
+inline Split sddmm_split(const SlotTiling &t, int64_t ntiles) {
+    const int64_t pk = std::max<int64_t>(t.P * t.K, 1);
+    int64_t ns = std::max<int64_t>(1, std::min<int64_t>(sp::ceil_div(512, pk), ntiles));
+    const int64_t tps = std::max<int64_t>(1, sp::ceil_div(ntiles, ns));
+    ns = std::max<int64_t>(1, sp::ceil_div(ntiles, tps));
+    return Split{(int)ns, (int)tps};
+}
+// Floats per split in the SDDMM partial buffer.
+inline int64_t part_stride(const SlotTiling &t) { return (t.nblk_cap + 1) * BLK; }
+
+// grad[e] = sum over the splits of part[split][pos] for the position pos of
+// entry e in the metadata blocks (fixed order; padding positions skipped).
+sp_status slot_reduce(const SlotTiling &t, const float *part, int nsplit, int64_t pstride, float *grad, hipStream_t st);
 
 }  // namespace spt2
