@@ -49,8 +49,8 @@ def parse():
 
 
 COPY_BYTES = 1 << 30
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm_k_sddmm_ffn_pair_hbm_traffic.txt")
-KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_tiled.h", "sp_tiling.hip", "sp_linear.hip"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm2_k_sddmm2_ffn_pair_hbm_traffic.txt")
+KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", "sp_linear.hip"]
 
 
 def kernel_source_hash():
@@ -211,9 +211,9 @@ def main():
     spmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k in ("fwd", "bwd_input")])
     sddmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k == "bwd_weight"])
     if 2 * sddmm_ms >= 4 * spmm_ms:
-        dom, dom_ms, kind = "k_sddmm+k_sddmm_reduce", sddmm_ms, "bwd_weight"
+        dom, dom_ms, kind = "k_sddmm2+k_slot_reduce", sddmm_ms, "bwd_weight"
     else:
-        dom, dom_ms, kind = "k_spmm", spmm_ms, "fwd"
+        dom, dom_ms, kind = "k_spmm2", spmm_ms, "fwd"
     fl = 2.0 * L1.nnz * B
     by = linear_alg_bytes(kind, B, L1.in_f, L1.out_f, L1.nnz)
     achieved_tf = fl / (dom_ms * 1e-3) / 1e12

@@ -292,6 +292,13 @@ __device__ inline float dot4(const float (&d)[4], const float4 &x) {
     return fmaf(d[3], x.w, v);
 }
 
+// First metadata word of block jb of a slot whose nb blocks start at bs.
+// Rounds past the slot's last block (another wave of the workgroup has more)
+// read block bs + nb instead: at most the first padding block after the
+// tiling's last one, so the read stays inside the metadata array; its value
+// is never used.
+__device__ inline int64_t slot_block(int bs, int nb, int jb) { return (int64_t)(bs + min(jb, nb)) * BLK; }
+
 // Geometry addition for the SDDMM:
 //   float4 load_dq(tok, t0, row0, s)   D[t0 + lane][rows of slot s of groups 0..3 of this wave]
 template <class Geo>
@@ -363,7 +370,7 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
             float4 dqn = geo.load_dq(tok, t0, row0, 0);
             int offn[JMAX];
 #pragma unroll
-            for (int jj = 0; jj < JMAX; ++jj) offn[jj] = tv.meta[(int64_t)(bs[0] + rho * JMAX + jj) * BLK + lp].x;
+            for (int jj = 0; jj < JMAX; ++jj) offn[jj] = tv.meta[slot_block(bs[0], nb[0], rho * JMAX + jj) + lp].x;
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 // keep each slot's loads where they are: hoisting all slots'
@@ -377,7 +384,7 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
                     dqn = geo.load_dq(tok, t0, row0, s + 1);
 #pragma unroll
                     for (int jj = 0; jj < JMAX; ++jj)
-                        offn[jj] = tv.meta[(int64_t)(bs[s + 1] + rho * JMAX + jj) * BLK + lp].x;
+                        offn[jj] = tv.meta[slot_block(bs[s + 1], nb[s + 1], rho * JMAX + jj) + lp].x;
                 }
                 sc[0 * T + lane] = dq.x;
                 sc[1 * T + lane] = dq.y;
