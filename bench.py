@@ -6,14 +6,25 @@ shaped sparse pair -- W1 768->3072 and W2 3072->768, each 95% unstructured
 sparse, 8192 tokens -- chained X -> W1 -> W2, then backward through W2 and W1
 (input gradient and weight gradient of each).  Six sparse ops per step.
 
-Metric: effective GFLOP/s = sum over ops of 2 * nnz * tokens, divided by the
-step time.  Inputs live in HBM before the timed region; the mask structure
-(plan) is prepared once outside it, as the method prescribes (masks change
-rarely), and its preparation time is reported separately.
+Other workloads (``--workload``), each timed the same way:
+  linear_small  a 256x256 linear layer at 90%, 16 tokens (latency-bound);
+  conv3x3_56    a 3x3 64->64 convolution on 32x64x56x56 at 90%;
+  conv_sweep    3x3 128@28x28, 3x3 256@14x14 and 1x1 256->1024@14x14 at batch 32,
+                each at 80/90/95/98%;
+  resnet18      the 20 convolutions and the FC layer of a ResNet-18 at batch 64,
+                224x224, 95% (sparse passes only; activations drawn per layer).
+A step is the forward, input gradient and weight gradient of every layer.
+
+Metric: effective GFLOP/s = sum over ops of 2 * nnz * tokens (linear) or
+2 * nnz * B * OH * OW (conv), divided by the step time.  Inputs live in HBM
+before the timed region; the mask structure (plan) is prepared once outside
+it, as the method prescribes (masks change rarely), and its preparation time
+is reported separately.
 
 Prints ONE JSON line.  Extra fields: `roofline` (dominant kernel: algorithmic
 bytes / FLOPs per launch over its event-timed duration), `cpu_baseline` (the
-CPU oracle timed on the host over whole repeated steps, about 10 s), `ops` (per-op times).
+CPU oracle timed on the host over a bounded sample, about 10 s), `ops`
+(per-op times).
 """
 from __future__ import annotations
 
@@ -33,6 +44,7 @@ HBM_PEAK_GBS = 8000.0
 # FP32 FMA on the vector ALUs, one FMA per lane per clock (packed FP32 is not
 # used): 256 CUs x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz.
 VALU_FP32_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+WORKLOADS = ("ffn", "linear_small", "conv3x3_56", "conv_sweep", "resnet18")
 
 
 def parse():
@@ -40,9 +52,10 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", choices=WORKLOADS, default="ffn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
-                    help="minimum CPU time of the oracle baseline (whole steps are repeated)")
+                    help="minimum CPU time of the oracle baseline (whole sample passes are repeated)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run only a plain device-to-device copy of COPY_BYTES (counter calibration)")
     return ap.parse_args()
@@ -54,7 +67,7 @@ KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", 
 
 
 def kernel_source_hash():
-    """sha256 over the sources of the kernels the bench launches."""
+    """sha256 over the sources of the kernels the FFN bench launches."""
     import hashlib
     h = hashlib.sha256()
     for f in KERNEL_SOURCES:
@@ -90,6 +103,8 @@ def calibrate_copy():
     print(json.dumps({"copy_bytes_read": COPY_BYTES, "copy_bytes_written": COPY_BYTES, "launches": 5}), flush=True)
 
 
+# ------------------------------------------------------------ algorithmic cost
+
 def linear_alg_bytes(op, B, in_f, out_f, nnz):
     """Minimum bytes an op must move: dense operands once, values+indices once."""
     if op == "fwd":
@@ -99,8 +114,25 @@ def linear_alg_bytes(op, B, in_f, out_f, nnz):
     return 4 * B * (in_f + out_f) + 8 * nnz + 4 * (out_f + 1)
 
 
-class Layer:
-    def __init__(self, sp, torch, d):
+def conv_alg_bytes(B, IC, H, W, OC, OH, OW, nnz):
+    """Activations once, then per stored entry a 4-byte value (forward, input
+    gradient) or a 4-byte gradient (weight gradient) plus its two 1-byte
+    taps, and the two index arrays of the format.  The same for all three
+    passes."""
+    return 4 * B * IC * H * W + 4 * B * OC * OH * OW + 6 * nnz + 2 * OC * (IC + 1) + 4 * (OC + 1)
+
+
+def bound_of(flops, nbytes):
+    """Roofline bound of an op: HBM when its arithmetic intensity is below the
+    ridge point (peak FLOP/s over peak B/s), else the FP32 ALU."""
+    return "hbm" if flops / nbytes * HBM_PEAK_GBS * 1e9 < VALU_FP32_PEAK_TFLOPS * 1e12 else "alu"
+
+
+# --------------------------------------------------------------------- layers
+
+class LinearLayer:
+    def __init__(self, sp, torch, d, name):
+        self.name = name
         self.out_f, self.in_f = d["mask"].shape
         dev = "cuda"
         m = torch.from_numpy(d["mask"]).to(dev)
@@ -108,8 +140,8 @@ class Layer:
         self.row_ptr = torch.empty(self.out_f + 1, dtype=torch.int32, device=dev)
         sp.sp_linear_encode_rows(self.out_f, self.in_f, m, self.row_ptr)
         self.nnz = int(self.row_ptr[-1].item())
-        self.col_idx = torch.empty(self.nnz, dtype=torch.int32, device=dev)
-        self.vals = torch.empty(self.nnz, dtype=torch.float32, device=dev)
+        self.col_idx = torch.empty(max(self.nnz, 1), dtype=torch.int32, device=dev)
+        self.vals = torch.empty(max(self.nnz, 1), dtype=torch.float32, device=dev)
         sp.sp_linear_encode_fill(self.out_f, self.in_f, m, w, self.row_ptr, self.col_idx, self.vals)
         self.plan = torch.empty(sp.sp_linear_plan_bytes(self.in_f, self.out_f, self.nnz), dtype=torch.uint8,
                                 device=dev)
@@ -118,7 +150,379 @@ class Layer:
         sp.sp_linear_plan(self.in_f, self.out_f, self.row_ptr, self.col_idx, self.nnz, self.plan)
         torch.cuda.synchronize()
         self.plan_ms = (time.perf_counter() - t) * 1e3
-        self.dW = torch.empty(self.nnz, dtype=torch.float32, device=dev)
+        self.dW = torch.empty(max(self.nnz, 1), dtype=torch.float32, device=dev)
+
+
+class ConvLayer:
+    def __init__(self, sp, torch, spec, seed):
+        from synth import conv_layer
+        name, B, IC, H, W, OC, KH, KW, s, p, sparsity = spec
+        self.name = name
+        self.dims = (B, IC, H, W, OC, KH, KW)
+        self.shape = sp.conv_shape(B, IC, H, W, OC, KH, KW, (s, s), (p, p))
+        self.OH, self.OW = sp.sp_conv_out_hw(self.shape)
+        d = conv_layer(seed, B, IC, H, W, OC, KH, KW, (self.OH, self.OW), sparsity)
+        dev = "cuda"
+        m = torch.from_numpy(d["mask"]).to(dev)
+        w = torch.from_numpy(d["W"]).to(dev)
+        self.w_oc = torch.empty(OC + 1, dtype=torch.int32, device=dev)
+        self.w_ic = torch.empty(OC * (IC + 1), dtype=torch.int16, device=dev)
+        sp.sp_conv_encode_rows(OC, IC, KH, KW, m, self.w_oc, self.w_ic)
+        self.nnz = int(self.w_oc[-1].item())
+        n1 = max(self.nnz, 1)
+        self.w_x = torch.empty(n1, dtype=torch.uint8, device=dev)
+        self.w_y = torch.empty(n1, dtype=torch.uint8, device=dev)
+        self.w_vals = torch.empty(n1, dtype=torch.float32, device=dev)
+        sp.sp_conv_encode_fill(OC, IC, KH, KW, m, w, self.w_oc, self.w_ic, self.w_x, self.w_y, self.w_vals)
+        self.plan = torch.empty(sp.sp_conv_plan_bytes(self.shape, self.nnz), dtype=torch.uint8, device=dev)
+        torch.cuda.synchronize()
+        t = time.perf_counter()
+        sp.sp_conv_plan(self.shape, self.w_oc, self.w_ic, self.w_x, self.w_y, self.nnz, self.plan)
+        torch.cuda.synchronize()
+        self.plan_ms = (time.perf_counter() - t) * 1e3
+        self.X = torch.from_numpy(d["X"]).to(dev)
+        self.dY = torch.from_numpy(d["dY"]).to(dev)
+        self.Y = torch.empty(B, OC, self.OH, self.OW, device=dev)
+        self.dX = torch.empty(B, IC, H, W, device=dev)
+        self.dW = torch.empty(n1, device=dev)
+        self.ws = torch.empty(max(sp.sp_conv_bwd_weight_ws(self.shape, self.nnz), 1), dtype=torch.uint8,
+                              device=dev)
+        self.mask_np, self.W_np = d["mask"], d["W"]
+
+    def ops(self, sp):
+        B, IC, H, W, OC, KH, KW = self.dims
+        fl = 2.0 * self.nnz * B * self.OH * self.OW
+        by = conv_alg_bytes(B, IC, H, W, OC, self.OH, self.OW, self.nnz)
+        return [
+            (self.name + ".fwd", lambda: sp.sp_conv_fwd(self.X, self.shape, self.w_vals, self.nnz, self.plan, self.Y),
+             "fwd", fl, by, self),
+            (self.name + ".bwd_input",
+             lambda: sp.sp_conv_bwd_input(self.dY, self.shape, self.w_vals, self.nnz, self.plan, self.dX),
+             "bwd_input", fl, by, self),
+            (self.name + ".bwd_weight",
+             lambda: sp.sp_conv_bwd_weight(self.dY, self.X, self.shape, self.nnz, self.plan, self.dW, self.ws),
+             "bwd_weight", fl, by, self),
+        ]
+
+
+# --------------------------------------------------------------------- timing
+
+def time_ops(torch, ops, steps, warmup):
+    """W untimed steps, then K steps between two events on the launch stream,
+    with an event pair around every op inside the timed region.  Returns the
+    step time (ms) and the mean time of every op (ms)."""
+    def step():
+        for op in ops:
+            op[1]()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0 = torch.cuda.Event(enable_timing=True)
+    e1 = torch.cuda.Event(enable_timing=True)
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for k in range(steps):
+        for op, (a, b) in zip(ops, evs[k]):
+            a.record(stream)
+            op[1]()
+            b.record(stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    per_op = [0.0] * len(ops)
+    for k in range(steps):
+        for i, (a, b) in enumerate(evs[k]):
+            per_op[i] += a.elapsed_time(b)
+    return e0.elapsed_time(e1) / steps, [t / steps for t in per_op]
+
+
+def op_row(ms, fl, by):
+    return {"ms": round(ms, 5), "tflops": round(fl / ms / 1e9, 3), "alg_GBps": round(by / ms / 1e6, 1),
+            "hbm_frac": round(by / ms / 1e6 / HBM_PEAK_GBS, 4), "bound": bound_of(fl, by)}
+
+
+def roofline(kernel, kind, fl, by, ms, traffic=None, extra=None):
+    """Roofline record of one kernel from its algorithmic flops/bytes per
+    launch and its mean event-timed launch duration (ms)."""
+    bound = bound_of(fl, by)
+    if bound == "alu":
+        achieved, peak, unit = fl / (ms * 1e-3) / 1e12, VALU_FP32_PEAK_TFLOPS, "TFLOP/s"
+    else:
+        achieved, peak, unit = by / (ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"
+    r = {"kernel": kernel, "op": kind, "bound": bound, "achieved": round(achieved, 3), "peak": round(peak, 1),
+         "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic,
+         "alg_bytes_per_launch": int(by), "flops_per_launch": fl, "ms_per_launch": round(float(ms), 5),
+         "hbm_achieved_GBps": round(by / (ms * 1e-3) / 1e9, 1), "hbm_peak_GBps": HBM_PEAK_GBS,
+         "hbm_frac": round(by / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+         "tflops": round(fl / (ms * 1e-3) / 1e12, 3), "alu_peak_TFLOPs": round(VALU_FP32_PEAK_TFLOPS, 1)}
+    if extra:
+        r.update(extra)
+    return r
+
+
+def base_record(args, value, ms_per_step, config):
+    return {
+        "metric": METRIC, "value": round(value, 1), "unit": "GFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "f32", "data": "synthetic", "config": config,
+    }
+
+
+def hbm_record(bytes_step, ms_per_step):
+    return {"alg_GB_per_step": round(bytes_step / 1e9, 4),
+            "achieved_GBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9, 1),
+            "frac_of_8TBps": round(bytes_step / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
+
+
+# ------------------------------------------------------------------ workloads
+
+def run_linear(args, sp, torch, which):
+    from synth import FFN_PAIR, LINEAR_SMALL, linear_layer, seed_for
+
+    if which == "ffn":
+        layers_np = [linear_layer(seed_for(2, li), o, i, B, s) for li, (_, o, i, B, s) in enumerate(FFN_PAIR)]
+        B = FFN_PAIR[0][3]
+    else:
+        layers_np = [linear_layer(seed_for(1, 0), o, i, B, s) for (_, o, i, B, s) in LINEAR_SMALL]
+        B = LINEAR_SMALL[0][3]
+    L1 = LinearLayer(sp, torch, layers_np[0], "W1")
+    X = torch.from_numpy(layers_np[0]["X"]).cuda()
+    Y1 = torch.empty(B, L1.out_f, device="cuda")
+    dX1 = torch.empty(B, L1.in_f, device="cuda")
+    if which == "ffn":
+        L2 = LinearLayer(sp, torch, layers_np[1], "W2")
+        dY2 = torch.from_numpy(layers_np[1]["dY"]).cuda()
+        Y2 = torch.empty(B, L2.out_f, device="cuda")
+        dX2 = torch.empty(B, L2.in_f, device="cuda")
+        layers = (L1, L2)
+    else:
+        dY1 = torch.from_numpy(layers_np[0]["dY"]).cuda()
+        layers = (L1,)
+    ws_bytes = max(max(sp.sp_linear_bwd_weight_ws(B, L.in_f, L.out_f, L.nnz) for L in layers), 1)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+
+    def lin_op(name, L, kind, f):
+        return (name, f, kind, 2.0 * L.nnz * B, linear_alg_bytes(kind, B, L.in_f, L.out_f, L.nnz), L)
+
+    if which == "ffn":
+        ops = [
+            lin_op("W1.fwd", L1, "fwd",
+                   lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
+            lin_op("W2.fwd", L2, "fwd",
+                   lambda: sp.sp_linear_fwd(Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, Y2)),
+            lin_op("W2.bwd_input", L2, "bwd_input",
+                   lambda: sp.sp_linear_bwd_input(dY2, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, dX2)),
+            lin_op("W2.bwd_weight", L2, "bwd_weight",
+                   lambda: sp.sp_linear_bwd_weight(dY2, Y1, B, L2.in_f, L2.out_f, L2.nnz, L2.plan, L2.dW, ws)),
+            lin_op("W1.bwd_input", L1, "bwd_input",
+                   lambda: sp.sp_linear_bwd_input(dX2, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1)),
+            lin_op("W1.bwd_weight", L1, "bwd_weight",
+                   lambda: sp.sp_linear_bwd_weight(dX2, X, B, L1.in_f, L1.out_f, L1.nnz, L1.plan, L1.dW, ws)),
+        ]
+    else:
+        ops = [
+            lin_op("fwd", L1, "fwd",
+                   lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
+            lin_op("bwd_input", L1, "bwd_input",
+                   lambda: sp.sp_linear_bwd_input(dY1, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1)),
+            lin_op("bwd_weight", L1, "bwd_weight",
+                   lambda: sp.sp_linear_bwd_weight(dY1, X, B, L1.in_f, L1.out_f, L1.nnz, L1.plan, L1.dW, ws)),
+        ]
+    ms_per_step, per_op = time_ops(torch, ops, args.steps, args.warmup)
+    flops_step = sum(o[3] for o in ops)
+    bytes_step = sum(o[4] for o in ops)
+
+    # Dominant kernel: the SpMM kernel serves fwd and bwd_input (equal
+    # algorithmic work per launch); the SDDMM kernel serves bwd_weight.
+    spmm = [t for o, t in zip(ops, per_op) if o[2] in ("fwd", "bwd_input")]
+    sddmm = [t for o, t in zip(ops, per_op) if o[2] == "bwd_weight"]
+    if sum(sddmm) >= sum(spmm):
+        dom, dom_ms, kind = "k_sddmm2+k_slot_reduce", float(np.mean(sddmm)), "bwd_weight"
+    else:
+        dom, dom_ms, kind = "k_spmm2", float(np.mean(spmm)), "fwd"
+    fl = 2.0 * L1.nnz * B
+    by = linear_alg_bytes(kind, B, L1.in_f, L1.out_f, L1.nnz)
+    traffic = measured_traffic(dom) if which == "ffn" else None
+    if which == "ffn":
+        config = {"workload": "FFN pair W1 768->3072 + W2 3072->768, 95% unstructured sparse, 8192 tokens, "
+                              "fwd+bwd (input and weight gradient) of both layers",
+                  "tokens": B, "sparsity": 0.95, "nnz_per_layer": L1.nnz}
+    else:
+        config = {"workload": "linear 256->256, 90% unstructured sparse, 16 tokens, fwd+bwd",
+                  "tokens": B, "sparsity": 0.90, "nnz": L1.nnz}
+    out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
+    out["hbm"] = hbm_record(bytes_step, ms_per_step)
+    out["roofline"] = roofline(dom, kind, fl, by, dom_ms, traffic, {"source_hash": kernel_source_hash()})
+    out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    out["plan_ms"] = {L.name: round(L.plan_ms, 3) for L in layers}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_linear(layers_np, args.cpu_seconds, which)
+    return out
+
+
+def conv_specs(which):
+    from synth import CONV_3X3_56, conv_sweep, resnet18_convs, seed_for
+    if which == "conv3x3_56":
+        return [(s, seed_for(3, i)) for i, s in enumerate(CONV_3X3_56)]
+    if which == "conv_sweep":
+        return [(s, seed_for(4, i)) for i, s in enumerate(conv_sweep())]
+    return [(s, seed_for(5, i)) for i, s in enumerate(resnet18_convs())]
+
+
+CONV_DESC = {
+    "conv3x3_56": "sparse 3x3 conv 64->64, stride 1, pad 1, input 32x64x56x56, 90% unstructured; fwd, bwd_input, "
+                  "bwd_weight",
+    "conv_sweep": "sparse conv sweep at batch 32: 3x3 128->128 @28x28, 3x3 256->256 @14x14, 1x1 256->1024 @14x14, "
+                  "each at 80/90/95/98%; fwd, bwd_input, bwd_weight of every layer",
+    "resnet18": "ResNet-18 sparse layers at batch 64, 224x224, 95%: the 20 convolutions and the FC 512->1000; "
+                "fwd, bwd_input, bwd_weight of every layer (BN/ReLU/pooling not included)",
+}
+CONV_KERNEL = {"fwd": "k_spmm<ConvGeo<0>>", "bwd_input": "k_spmm<ConvGeo<1|2>>",
+               "bwd_weight": "k_sddmm<ConvGeo<0>>+k_sddmm_reduce"}
+
+
+def run_conv(args, sp, torch, which):
+    from synth import RESNET18_FC, linear_layer, seed_for
+    layers = []
+    for spec, seed in conv_specs(which):
+        layers.append(ConvLayer(sp, torch, spec, seed))
+    ops = []
+    for L in layers:
+        ops += L.ops(sp)
+    fc = None
+    if which == "resnet18":
+        _, o_f, i_f, B, s = RESNET18_FC
+        d = linear_layer(seed_for(5, 20), o_f, i_f, B, s)
+        fc = LinearLayer(sp, torch, d, "fc")
+        X = torch.from_numpy(d["X"]).cuda()
+        dY = torch.from_numpy(d["dY"]).cuda()
+        Y = torch.empty(B, o_f, device="cuda")
+        dX = torch.empty(B, i_f, device="cuda")
+        ws = torch.empty(max(sp.sp_linear_bwd_weight_ws(B, i_f, o_f, fc.nnz), 1), dtype=torch.uint8, device="cuda")
+        for kind, f in (("fwd", lambda: sp.sp_linear_fwd(X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, Y)),
+                        ("bwd_input", lambda: sp.sp_linear_bwd_input(dY, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, dX)),
+                        ("bwd_weight", lambda: sp.sp_linear_bwd_weight(dY, X, B, i_f, o_f, fc.nnz, fc.plan, fc.dW,
+                                                                       ws))):
+            ops.append(("fc." + kind, f, kind, 2.0 * fc.nnz * B, linear_alg_bytes(kind, B, i_f, o_f, fc.nnz), fc))
+    ms_per_step, per_op = time_ops(torch, ops, args.steps, args.warmup)
+    flops_step = sum(o[3] for o in ops)
+    bytes_step = sum(o[4] for o in ops)
+    # Dominant kernel: the conv op kind with the largest total time; its
+    # roofline is taken per launch as total work over total time of its launches.
+    kinds = {}
+    for o, t in zip(ops, per_op):
+        if isinstance(o[5], ConvLayer):
+            k = kinds.setdefault(o[2], [0.0, 0.0, 0.0, 0])
+            k[0] += t
+            k[1] += o[3]
+            k[2] += o[4]
+            k[3] += 1
+    kind = max(kinds, key=lambda k: kinds[k][0])
+    t, fl, by, n = kinds[kind]
+    config = {"workload": CONV_DESC[which], "layers": len(layers) + (1 if fc else 0),
+              "nnz_total": int(sum(L.nnz for L in layers) + (fc.nnz if fc else 0))}
+    out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
+    out["hbm"] = hbm_record(bytes_step, ms_per_step)
+    out["roofline"] = roofline(CONV_KERNEL[kind], kind, fl / n, by / n, t / n, None,
+                               {"launches_per_step": n, "note": "per-launch means over the workload's layers"})
+    out["by_op"] = {k: {"ms": round(v[0], 4), "tflops": round(v[1] / v[0] / 1e9, 3),
+                        "alg_GBps": round(v[2] / v[0] / 1e6, 1), "bound": bound_of(v[1], v[2])}
+                    for k, v in kinds.items()}
+    out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    out["plan_ms"] = {L.name: round(L.plan_ms, 3) for L in layers}
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_conv(layers, args.cpu_seconds)
+    return out
+
+
+# --------------------------------------------------------------- CPU baseline
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
+
+
+def cpu_baseline_linear(layers_np, min_seconds, which):
+    """The CPU oracle (as it stands) on the same step over all tokens,
+    repeated until at least `min_seconds` have passed; reported in the same
+    effective-GFLOP/s unit."""
+    import oracle
+    X = layers_np[0]["X"]
+    ntok = X.shape[0]
+    enc = [oracle.linear_encode(d["mask"], d["W"]) for d in layers_np]
+    reps = 0
+    t = time.perf_counter()
+    while True:
+        if which == "ffn":
+            (rp1, ci1, v1), (rp2, ci2, v2) = enc
+            o1, i1 = layers_np[0]["mask"].shape
+            o2, i2 = layers_np[1]["mask"].shape
+            dY2 = layers_np[1]["dY"]
+            Y1, _ = oracle.linear_fwd(X, rp1, ci1, v1, o1)
+            Y1f = Y1.astype(np.float32)
+            oracle.linear_fwd(Y1f, rp2, ci2, v2, o2)
+            dX2, _ = oracle.linear_bwd_input(dY2, rp2, ci2, v2, i2)
+            oracle.linear_bwd_weight(dY2, Y1f, rp2, ci2)
+            dX2f = dX2.astype(np.float32)
+            oracle.linear_bwd_input(dX2f, rp1, ci1, v1, i1)
+            oracle.linear_bwd_weight(dX2f, X, rp1, ci1)
+        else:
+            (rp1, ci1, v1), = enc
+            o1, i1 = layers_np[0]["mask"].shape
+            oracle.linear_fwd(X, rp1, ci1, v1, o1)
+            oracle.linear_bwd_input(layers_np[0]["dY"], rp1, ci1, v1, i1)
+            oracle.linear_bwd_weight(layers_np[0]["dY"], X, rp1, ci1)
+        reps += 1
+        t_total = time.perf_counter() - t
+        if t_total >= min_seconds:
+            break
+    flops = reps * 3 * 2.0 * sum(len(e[2]) for e in enc) * ntok
+    return {"value": round(flops / t_total / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(t_total, 2), "cpu": _cpu_model(),
+            "sample": "the same %d-op step over all %d tokens, repeated %d times (fp64-accumulating plain loops, "
+                      "OpenMP over independent outputs; conversions between ops included)"
+                      % (3 * len(enc), ntok, reps)}
+
+
+def cpu_baseline_conv(layers, min_seconds):
+    """The CPU oracle on one image per layer (forward, input gradient and
+    weight gradient of that image), cycling over the layers until at least
+    `min_seconds` have passed and every layer has run once."""
+    import oracle
+    from synth import conv_layer
+    samples = []
+    for i, L in enumerate(layers):
+        B, IC, H, W, OC, KH, KW = L.dims
+        s = L.shape
+        d1 = conv_layer(777 + i, 1, IC, H, W, OC, KH, KW, (L.OH, L.OW), 0.5)
+        enc = oracle.conv_encode(L.mask_np, L.W_np)
+        osh = oracle.conv_shape(1, IC, H, W, OC, KH, KW, (s.stride_h, s.stride_w), (s.pad_h, s.pad_w))
+        samples.append((d1["X"], d1["dY"], osh, enc, 3 * 2.0 * L.nnz * L.OH * L.OW))
+    flops, n = 0.0, 0
+    t = time.perf_counter()
+    while True:
+        X1, dY1, osh, enc, fl = samples[n % len(samples)]
+        oracle.conv_fwd(X1, osh, *enc)
+        oracle.conv_bwd_input(dY1, osh, *enc)
+        oracle.conv_bwd_weight(dY1, X1, osh, *enc[:4])
+        flops += fl
+        n += 1
+        t_total = time.perf_counter() - t
+        if t_total >= min_seconds and n >= len(samples):
+            break
+    return {"value": round(flops / t_total / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle", "seconds": round(t_total, 2), "cpu": _cpu_model(),
+            "sample": "forward, input gradient and weight gradient of one image per layer, %d layer passes over "
+                      "%d layers (fp64-accumulating plain loops, OpenMP over independent outputs)"
+                      % (n, len(samples))}
 
 
 def main():
@@ -137,164 +541,11 @@ def main():
         return
 
     import paper_2302_04852_amd as sp
-    from synth import linear_layer, FFN_PAIR, seed_for
-
-    layers_np = []
-    for li, (name, out_f, in_f, B, s) in enumerate(FFN_PAIR):
-        layers_np.append(linear_layer(seed_for(2, li), out_f, in_f, B, s))
-    B = FFN_PAIR[0][3]
-    L1 = Layer(sp, torch, layers_np[0])
-    L2 = Layer(sp, torch, layers_np[1])
-    X = torch.from_numpy(layers_np[0]["X"]).cuda()
-    dY2 = torch.from_numpy(layers_np[1]["dY"]).cuda()
-    Y1 = torch.empty(B, L1.out_f, device="cuda")
-    Y2 = torch.empty(B, L2.out_f, device="cuda")
-    dX2 = torch.empty(B, L2.in_f, device="cuda")
-    dX1 = torch.empty(B, L1.in_f, device="cuda")
-    ws_bytes = max(sp.sp_linear_bwd_weight_ws(B, L.in_f, L.out_f, L.nnz) for L in (L1, L2))
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
-
-    ops = [
-        ("W1.fwd", lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1), L1, "fwd"),
-        ("W2.fwd", lambda: sp.sp_linear_fwd(Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, Y2), L2, "fwd"),
-        ("W2.bwd_input", lambda: sp.sp_linear_bwd_input(dY2, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, dX2),
-         L2, "bwd_input"),
-        ("W2.bwd_weight", lambda: sp.sp_linear_bwd_weight(dY2, Y1, B, L2.in_f, L2.out_f, L2.nnz, L2.plan, L2.dW, ws),
-         L2, "bwd_weight"),
-        ("W1.bwd_input", lambda: sp.sp_linear_bwd_input(dX2, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1),
-         L1, "bwd_input"),
-        ("W1.bwd_weight", lambda: sp.sp_linear_bwd_weight(dX2, X, B, L1.in_f, L1.out_f, L1.nnz, L1.plan, L1.dW, ws),
-         L1, "bwd_weight"),
-    ]
-    flops_step = sum(2.0 * L.nnz * B for _, _, L, _ in ops)
-
-    def step():
-        for _, f, _, _ in ops:
-            f()
-
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-
-    # Timed region: K whole steps between two events on the launch stream,
-    # with an event pair around every op inside it (per-op durations).
-    stream = torch.cuda.current_stream()
-    e0 = torch.cuda.Event(enable_timing=True)
-    e1 = torch.cuda.Event(enable_timing=True)
-    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in ops]
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    e0.record(stream)
-    for k in range(args.steps):
-        for (name, f, _, _), (a, b) in zip(ops, evs[k]):
-            a.record(stream)
-            f()
-            b.record(stream)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    total_ms = e0.elapsed_time(e1)
-    ms_per_step = total_ms / args.steps
-    per_op = {name: 0.0 for name, _, _, _ in ops}
-    for k in range(args.steps):
-        for (name, _, _, _), (a, b) in zip(ops, evs[k]):
-            per_op[name] += a.elapsed_time(b)
-    op_rows = {}
-    for name, _, L, kind in ops:
-        ms = per_op[name] / args.steps
-        fl = 2.0 * L.nnz * B
-        by = linear_alg_bytes(kind, B, L.in_f, L.out_f, L.nnz)
-        op_rows[name] = {"ms": round(ms, 5), "tflops": round(fl / ms / 1e9, 3),
-                         "alg_GBps": round(by / ms / 1e6, 1), "hbm_frac": round(by / ms / 1e6 / HBM_PEAK_GBS, 4)}
-
-    # Dominant kernel: the SpMM kernel serves fwd and bwd_input (4 launches
-    # of equal algorithmic work per step); the SDDMM kernel serves bwd_weight.
-    spmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k in ("fwd", "bwd_input")])
-    sddmm_ms = np.mean([per_op[n] / args.steps for n, _, _, k in ops if k == "bwd_weight"])
-    if 2 * sddmm_ms >= 4 * spmm_ms:
-        dom, dom_ms, kind = "k_sddmm2+k_slot_reduce", sddmm_ms, "bwd_weight"
+    if args.workload in ("ffn", "linear_small"):
+        out = run_linear(args, sp, torch, args.workload)
     else:
-        dom, dom_ms, kind = "k_spmm2", spmm_ms, "fwd"
-    fl = 2.0 * L1.nnz * B
-    by = linear_alg_bytes(kind, B, L1.in_f, L1.out_f, L1.nnz)
-    achieved_tf = fl / (dom_ms * 1e-3) / 1e12
-    traffic = measured_traffic(dom)
-    roof = {"kernel": dom, "bound": "alu", "achieved": round(achieved_tf, 3), "peak": round(VALU_FP32_PEAK_TFLOPS, 1),
-            "unit": "TFLOP/s", "frac": round(achieved_tf / VALU_FP32_PEAK_TFLOPS, 4), "traffic": traffic,
-            "source_hash": kernel_source_hash(),
-            "alg_bytes_per_launch": by, "flops_per_launch": fl, "ms_per_launch": round(float(dom_ms), 5),
-            "hbm_achieved_GBps": round(by / (dom_ms * 1e-3) / 1e9, 1), "hbm_peak_GBps": HBM_PEAK_GBS,
-            "hbm_frac": round(by / (dom_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}
-
-    step_bytes = sum(linear_alg_bytes(k, B, L.in_f, L.out_f, L.nnz) for _, _, L, k in ops)
-    out = {
-        "metric": METRIC,
-        "value": round(flops_step / (ms_per_step * 1e-3) / 1e9, 1),
-        "unit": "GFLOP/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(ms_per_step, 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": "FFN pair W1 768->3072 + W2 3072->768, 95% unstructured sparse, 8192 tokens, "
-                               "fwd+bwd (input and weight gradient) of both layers",
-                   "tokens": B, "sparsity": 0.95, "nnz_per_layer": L1.nnz},
-        "hbm": {"alg_GB_per_step": round(step_bytes / 1e9, 4),
-                "achieved_GBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
-                "frac_of_8TBps": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
-        "roofline": roof,
-        "ops": op_rows,
-        "plan_ms": {"W1": round(L1.plan_ms, 3), "W2": round(L2.plan_ms, 3)},
-    }
-
-    if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(layers_np, args.cpu_seconds)
+        out = run_conv(args, sp, torch, args.workload)
     print(json.dumps(out), flush=True)
-
-
-def cpu_baseline(layers_np, min_seconds):
-    """The CPU oracle (as it stands) on the same six-op step over all tokens,
-    repeated until at least `min_seconds` have passed; reported in the same
-    effective-GFLOP/s unit."""
-    import oracle
-    X = layers_np[0]["X"]
-    dY2 = layers_np[1]["dY"]
-    ntok = X.shape[0]
-    (rp1, ci1, v1), (rp2, ci2, v2) = [oracle.linear_encode(d["mask"], d["W"]) for d in layers_np]
-    o1, i1 = layers_np[0]["mask"].shape
-    o2, i2 = layers_np[1]["mask"].shape
-    reps = 0
-    t = time.perf_counter()
-    while True:
-        Y1, _ = oracle.linear_fwd(X, rp1, ci1, v1, o1)
-        Y1f = Y1.astype(np.float32)
-        oracle.linear_fwd(Y1f, rp2, ci2, v2, o2)
-        dX2, _ = oracle.linear_bwd_input(dY2, rp2, ci2, v2, i2)
-        oracle.linear_bwd_weight(dY2, Y1f, rp2, ci2)
-        dX2f = dX2.astype(np.float32)
-        oracle.linear_bwd_input(dX2f, rp1, ci1, v1, i1)
-        oracle.linear_bwd_weight(dX2f, X, rp1, ci1)
-        reps += 1
-        t_total = time.perf_counter() - t
-        if t_total >= min_seconds:
-            break
-    flops = reps * 3 * 2.0 * (len(v1) + len(v2)) * ntok
-    cpu_model = ""
-    try:
-        for line in open("/proc/cpuinfo"):
-            if line.startswith("model name"):
-                cpu_model = line.split(":", 1)[1].strip()
-                break
-    except OSError:
-        pass
-    return {"value": round(flops / t_total / 1e9, 3), "unit": "GFLOP/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": round(t_total, 2), "cpu": cpu_model,
-            "sample": "the same six-op FFN step over all %d tokens, repeated %d times (fp64-accumulating "
-                      "plain loops, OpenMP over independent outputs; conversions between ops included)"
-                      % (ntok, reps)}
 
 
 if __name__ == "__main__":
