@@ -12,6 +12,15 @@
 //     input-channel-major view, tokens = input pixels (b, m, n),
 //     G[t][col] = dY[b, oc, (m+ph-x)/sh, (n+pw-y)/sw] where that divides
 //     exactly and lies inside dY, 0 elsewhere.
+//     With stride 2 in both directions the input pixels are split into four
+//     phases (m mod 2, n mod 2).  Only taps with x = m + ph and y = n + pw
+//     (mod 2) reach a phase, so each phase is a unit-stride gather over its
+//     own tap class: columns (oc, x div 2, y div 2) of the entries whose taps
+//     have that parity, tokens the phase's pixels.  No gather is wasted on a
+//     tap that cannot contribute.  Other strides use the general gather with
+//     the divisibility test.
+//     Layers with at most 8 input channels (image stems) use a direct kernel
+//     instead: a 16-wave tile would leave most waves without rows.
 // Within a row (channel) the format's (channel, x, y) order is exactly the
 // ascending column order, so the format itself is the CSR of the forward
 // tiling.  The gather uses raw buffer loads: an element outside the image
@@ -199,9 +208,12 @@ struct ConvGeo {
     int KH, KW, KK;
     int gH, gW, gplane, gimg;  // G: plane height/width, plane size, image size (elements)
     int sh, sw, ph, pw;
-    float *Out;       // SpMM output [images][orows][npix]
+    float *Out;       // SpMM output [images][orows][onpix]
     const float *D;   // SDDMM stationary operand, same layout as Out
     int orows;
+    // Output pixel of the token at grid position (r, s): (r*osh + oa)*oW + s*osw + ob
+    // (the identity map for the full pixel grid; a strided sub-grid for a phase).
+    int onpix, oW, osh, osw, oa, ob;
 
     struct Tok {
         int a, c;      // spatial origin of the staging token (see tile_init)
@@ -231,12 +243,13 @@ struct ConvGeo {
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
             const int ts = (int)t0 + (tid & 127) + 128 * h;
-            int ob = -1;
+            int o = -1;
             if (ts < ntok) {
-                const int b = ts / npix;
-                ob = b * orows * npix + (ts - b * npix);
+                const int b = ts / npix, pix = ts - b * npix;
+                const int r = pix / tw, c = pix - r * tw;
+                o = b * orows * onpix + (r * osh + oa) * oW + c * osw + ob;
             }
-            tk.obase[h] = ob;
+            tk.obase[h] = o;
         }
     }
 
@@ -304,7 +317,7 @@ struct ConvGeo {
             if (ob >= 0) {
                 for (int r = tid >> 7; r < R; r += NTHR / 128) {
                     const int64_t gr = row0 + r;
-                    if (gr < orows) Out[ob + gr * npix] = ys[r * YS + tl];
+                    if (gr < orows) Out[ob + gr * onpix] = ys[r * YS + tl];
                 }
             }
         }
@@ -321,7 +334,7 @@ struct ConvGeo {
             const int ob = tk.obase[h], tl = tid & 127;
             for (int r = tid >> 7; r < R; r += NTHR / 128) {
                 const int64_t gr = row0 + r;
-                ys[r * YS + tl] = (ob >= 0 && gr < orows) ? D[ob + gr * npix] : 0.f;
+                ys[r * YS + tl] = (ob >= 0 && gr < orows) ? D[ob + gr * onpix] : 0.f;
             }
             __syncthreads();
             if ((lane >> 5) == h) {
@@ -376,14 +389,41 @@ bool fits(const Dims &d) {
     return x <= (double)MAX_BYTES && y <= (double)MAX_BYTES;
 }
 
+// Tap class c = (x mod 2)*2 + (y mod 2) of a stride-2 layer: its taps are
+// x = cx + 2i (i < ncx), y = cy + 2j (j < ncy), its columns (oc, i, j).
+struct TapClass {
+    int cx, cy, ncx, ncy;
+};
+inline TapClass tap_class(int c, int KH, int KW) {
+    TapClass t;
+    t.cx = c >> 1;
+    t.cy = c & 1;
+    t.ncx = t.cx < KH ? (KH - 1 - t.cx) / 2 + 1 : 0;
+    t.ncy = t.cy < KW ? (KW - 1 - t.cy) / 2 + 1 : 0;
+    return t;
+}
+
+// Per tap class of a stride-2 input gradient: the class's entries as a CSR
+// over input channels (columns (oc, i, j) ascending, value index in src) and
+// its tiling.  Sized for up to nnz entries each, since the split of the
+// entries between the classes is known only on the device.
+struct ClassPart {
+    TapClass tc;
+    int32_t *ptr, *col, *src;
+    spt::Tiling T;
+};
+
 struct ConvPlan {
     int32_t *t_ic_ptr, *t_oc, *t_perm;
     int32_t *colA, *colB;
     spt::Tiling A, Bt;  // A: rows = OC, columns (ic, tap); Bt: rows = IC, columns (oc, tap)
+    ClassPart cls[4];   // stride-2 input gradient, one per tap class
     int32_t *cnt;
     size_t bytes;
 };
 
+// Plan layout: a function of (OC, IC, KH, KW, nnz) only, so one plan serves
+// every batch, spatial size, stride and padding.
 ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
     sp::Carve c(const_cast<void *>(base));
     ConvPlan L;
@@ -394,9 +434,91 @@ ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
     L.colB = c.take<int32_t>(nnz);
     spt::tiling_layout(c, L.A, d.OC, d.IC * d.KK, nnz);
     spt::tiling_layout(c, L.Bt, d.IC, d.OC * d.KK, nnz);
+    for (int k = 0; k < 4; ++k) {
+        ClassPart &cp = L.cls[k];
+        cp.tc = tap_class(k, d.KH, d.KW);
+        cp.ptr = c.take<int32_t>(d.IC + 1);
+        cp.col = c.take<int32_t>(nnz);
+        cp.src = c.take<int32_t>(nnz);
+        spt::tiling_layout(c, cp.T, d.IC, d.OC * cp.tc.ncx * cp.tc.ncy, nnz);
+    }
     L.cnt = c.take<int32_t>(std::max(d.OC * L.A.K, d.IC * L.Bt.K));
     L.bytes = c.off;
     return L;
+}
+
+// Per input channel, the number of its entries in each tap class.
+struct ClassOut {
+    int32_t *ptr[4], *col[4], *src[4];
+    int nc[4], ncy[4];  // columns per output channel, columns per tap row
+};
+
+__global__ __launch_bounds__(256) void k_cls_count(const int32_t *__restrict__ t_ic_ptr,
+                                                   const int32_t *__restrict__ t_perm, const uint8_t *__restrict__ w_x,
+                                                   const uint8_t *__restrict__ w_y, int64_t IC, ClassOut o) {
+    const int64_t ic = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ic >= IC) return;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int32_t n = 0;
+        for (int32_t j = t_ic_ptr[ic]; j < t_ic_ptr[ic + 1]; ++j) {
+            const int32_t si = t_perm[j];
+            n += ((w_x[si] & 1) * 2 + (w_y[si] & 1)) == k;
+        }
+        o.ptr[k][ic + 1] = n;
+    }
+}
+
+// Place every entry of the input-channel-major view in its class, keeping
+// the view's (oc, x, y) order, with column oc*nc + (x div 2)*ncy + (y div 2).
+__global__ __launch_bounds__(256) void k_cls_fill(const int32_t *__restrict__ t_ic_ptr,
+                                                  const int32_t *__restrict__ t_oc, const int32_t *__restrict__ t_perm,
+                                                  const uint8_t *__restrict__ w_x, const uint8_t *__restrict__ w_y,
+                                                  int64_t IC, ClassOut o) {
+    const int64_t ic = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ic >= IC) return;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        int32_t pos = o.ptr[k][ic];
+        for (int32_t j = t_ic_ptr[ic]; j < t_ic_ptr[ic + 1]; ++j) {
+            const int32_t si = t_perm[j];
+            const int x = w_x[si], y = w_y[si];
+            if ((x & 1) * 2 + (y & 1) != k) continue;
+            o.col[k][pos] = t_oc[j] * o.nc[k] + (x >> 1) * o.ncy[k] + (y >> 1);
+            o.src[k][pos] = si;
+            ++pos;
+        }
+    }
+}
+
+sp_status classes_build(const ConvPlan &L, const Dims &d, const uint8_t *w_x, const uint8_t *w_y, int64_t nnz,
+                        hipStream_t st) {
+    sp_status r;
+    for (int k = 0; k < 4; ++k)
+        if ((r = sp::fill_i32(L.cls[k].ptr, d.IC + 1, 0, st))) return r;
+    ClassOut o;
+    for (int k = 0; k < 4; ++k) {
+        o.ptr[k] = L.cls[k].ptr;
+        o.col[k] = L.cls[k].col;
+        o.src[k] = L.cls[k].src;
+        o.nc[k] = L.cls[k].tc.ncx * L.cls[k].tc.ncy;
+        o.ncy[k] = L.cls[k].tc.ncy;
+    }
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_cls_count, dim3((unsigned)sp::ceil_div(d.IC, 256)), dim3(256), 0, st, L.t_ic_ptr,
+                           L.t_perm, w_x, w_y, d.IC, o);
+        SP_CHECK_LAUNCH();
+    }
+    for (int k = 0; k < 4; ++k)
+        if ((r = sp::scan_counts(L.cls[k].ptr, d.IC, st))) return r;
+    if (nnz > 0) {
+        hipLaunchKernelGGL(k_cls_fill, dim3((unsigned)sp::ceil_div(d.IC, 256)), dim3(256), 0, st, L.t_ic_ptr,
+                           L.t_oc, L.t_perm, w_x, w_y, d.IC, o);
+        SP_CHECK_LAUNCH();
+    }
+    for (int k = 0; k < 4; ++k)
+        if ((r = spt::tiling_build(L.cls[k].T, L.cls[k].ptr, L.cls[k].col, L.cls[k].src, L.cnt, st))) return r;
+    return SP_OK;
 }
 
 template <int DIR>
@@ -432,6 +554,36 @@ ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
         g.gbytes = (int)(d.B * d.OC * d.OH * d.OW * 4);
         g.orows = (int)d.IC;
     }
+    g.onpix = g.npix;
+    g.oW = g.tw;
+    g.osh = g.osw = 1;
+    g.oa = g.ob = 0;
+    return g;
+}
+
+// Input-gradient geometry of phase (a, b) of a stride-2 layer: tokens are the
+// input pixels (img, 2m'+a, 2n'+b); the phase uses tap class
+// ((a+ph) mod 2, (b+pw) mod 2), whose tap (cx+2i, cy+2j) reads dY at
+// (m' + A0 - i, n' + B0 - j) with A0 = (a+ph-cx)/2, B0 = (b+pw-cy)/2: a
+// unit-stride gather (DIR 1) with the class as kernel and (A0, B0) as padding.
+ConvGeo<1> phase_geo(const Dims &d, int a, int b, const TapClass &tc) {
+    ConvGeo<1> g = make_geo<1>(d, false);
+    const int hm = a < d.H ? (int)((d.H - 1 - a) / 2 + 1) : 0;
+    const int wn = b < d.W ? (int)((d.W - 1 - b) / 2 + 1) : 0;
+    g.ntok = (int)(d.B * hm * wn);
+    g.npix = hm * wn;
+    g.tw = wn;
+    g.KH = tc.ncx;
+    g.KW = tc.ncy;
+    g.KK = tc.ncx * tc.ncy;
+    g.ncols = (int)(d.OC * g.KK);
+    g.ph = (a + d.ph - tc.cx) / 2;
+    g.pw = (b + d.pw - tc.cy) / 2;
+    g.onpix = (int)(d.H * d.W);
+    g.oW = (int)d.W;
+    g.osh = g.osw = 2;
+    g.oa = a;
+    g.ob = b;
     return g;
 }
 
@@ -449,6 +601,84 @@ sp_status spmm(const spt::Tiling &t, const Geo &geo, const float *vals, hipStrea
                            (int)ntiles);
     SP_CHECK_LAUNCH();
     return SP_OK;
+}
+
+// Direct input gradient for layers with at most FR_MAX input channels (image
+// stems): one thread per input pixel of the (phase) grid computes every
+// channel.  The channels' entries -- gather offset within dY, taps and value
+// -- are staged in LDS and read as wave-uniform broadcasts; dY is read
+// straight from global memory, neighbouring threads reading neighbouring
+// pixels.  A 16-wave tile would leave all but one wave without rows here.
+constexpr int FR_MAX = 8;
+constexpr int FR_ENT = 2048;  // entries staged per round (32 KB)
+
+__global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__restrict__ ptr,
+                                                 const int32_t *__restrict__ col, const int32_t *__restrict__ src,
+                                                 const float *__restrict__ vals, int nrows) {
+    __shared__ int4 ent[FR_ENT];
+    const int tid = threadIdx.x;
+    const int t = (int)blockIdx.x * 256 + tid;
+    int a = TOK_INVALID, c = TOK_INVALID, gbase = 0, obase = -1;
+    if (t < g.ntok) {
+        const int b = t / g.npix, pix = t - b * g.npix;
+        const int r = pix / g.tw, q = pix - r * g.tw;
+        a = r + g.ph;
+        c = q + g.pw;
+        gbase = b * g.gimg + a * g.gW + c;
+        obase = b * g.orows * g.onpix + (r * g.osh + g.oa) * g.oW + q * g.osw + g.ob;
+    }
+    const sp_i32x4 rsrc = sp::make_rsrc(g.G, (uint32_t)g.gbytes);
+    const int e_all = ptr[nrows] - ptr[0];
+    float acc[FR_MAX];
+#pragma unroll
+    for (int r = 0; r < FR_MAX; ++r) acc[r] = 0.f;
+    for (int e0 = 0; e0 < e_all; e0 += FR_ENT) {
+        const int ne = min(FR_ENT, e_all - e0);
+        __syncthreads();
+        for (int i = tid; i < ne; i += 256) {
+            const int j = ptr[0] + e0 + i;
+            const int cc = col[j];
+            const int oc = cc / g.KK, tap = cc - oc * g.KK;
+            const int ix = tap / g.KW, iy = tap - ix * g.KW;
+            ent[i] = make_int4(oc * g.gplane - ix * g.gW - iy, ix, iy, __float_as_int(vals[src[j]]));
+        }
+        __syncthreads();
+#pragma unroll
+        for (int r = 0; r < FR_MAX; ++r) {
+            if (r < nrows) {
+                const int j0 = max(ptr[r] - ptr[0] - e0, 0), j1 = min(ptr[r + 1] - ptr[0] - e0, ne);
+                for (int j = j0; j < j1; ++j) {
+                    const int4 e = ent[j];
+                    const bool ok = (unsigned)(a - e.y) < (unsigned)g.gH && (unsigned)(c - e.z) < (unsigned)g.gW;
+                    const float x = sp_raw_buffer_load_f32(rsrc, ok ? (gbase + e.x) * 4 : OOB, 0, 0);
+                    acc[r] = fmaf(__int_as_float(e.w), x, acc[r]);
+                }
+            }
+        }
+    }
+    if (obase >= 0) {
+#pragma unroll
+        for (int r = 0; r < FR_MAX; ++r)
+            if (r < nrows) g.Out[obase + r * g.onpix] = acc[r];
+    }
+}
+
+sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, const int32_t *src, const float *vals,
+                  int nrows, hipStream_t st) {
+    if (g.ntok == 0) return SP_OK;
+    hipLaunchKernelGGL(k_fewrows, dim3((unsigned)sp::ceil_div(g.ntok, 256)), dim3(256), 0, st, g, ptr, col, src, vals,
+                       nrows);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
+// Input gradient of one unit-stride problem (the whole layer at stride 1, or
+// one phase of a stride-2 layer) over a CSR by input channel and its tiling.
+sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt::Tiling &t, const int32_t *ptr,
+                         const int32_t *col, const int32_t *src, const float *vals, hipStream_t st) {
+    if (g.ntok == 0) return SP_OK;
+    if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, st);
+    return spmm(t, g, vals, st);
 }
 
 int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, T); }
@@ -520,7 +750,8 @@ extern "C" sp_status sp_conv_plan(const sp_conv_shape *s, const int32_t *w_oc, c
         SP_CHECK_LAUNCH();
     }
     if ((r = spt::tiling_build(L.A, w_oc, L.colA, nullptr, L.cnt, st))) return r;
-    return spt::tiling_build(L.Bt, L.t_ic_ptr, L.colB, L.t_perm, L.cnt, st);
+    if ((r = spt::tiling_build(L.Bt, L.t_ic_ptr, L.colB, L.t_perm, L.cnt, st))) return r;
+    return classes_build(L, d, w_x, w_y, nnz, st);
 }
 
 extern "C" sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const float *w_vals, int64_t nnz,
@@ -555,7 +786,18 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         ConvGeo<1> g = make_geo<1>(d, false);
         g.G = dY;
         g.Out = dX;
-        return spmm(L.Bt, g, w_vals, st);
+        return bwd_input_part(d, g, L.Bt, L.t_ic_ptr, L.colB, L.t_perm, w_vals, st);
+    }
+    if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
+        for (int a = 0; a < 2; ++a)
+            for (int b = 0; b < 2; ++b) {
+                const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
+                ConvGeo<1> g = phase_geo(d, a, b, cp.tc);
+                g.G = dY;
+                g.Out = dX;
+                if ((r = bwd_input_part(d, g, cp.T, cp.ptr, cp.col, cp.src, w_vals, st))) return r;
+            }
+        return SP_OK;
     }
     ConvGeo<2> g = make_geo<2>(d, false);
     g.G = dY;
@@ -568,7 +810,10 @@ extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, 
     if (!bytes) return SP_ERR_INVALID_ARG;
     sp_status r = dims_of(s, nnz, d);
     if (r) return r;
-    *bytes = (nnz > 0 && d.B > 0) ? sp::align256((size_t)wgrad_tiles(d) * (size_t)spt::padded_cap(nnz) * 4) : 0;
+    const int64_t nt = wgrad_tiles(d);
+    *bytes = (nnz > 0 && d.B > 0)
+                 ? sp::align256((size_t)(nt + spt::reduce_blocks(nt)) * (size_t)spt::padded_cap(nnz) * 4)
+                 : 0;
     return SP_OK;
 }
 
@@ -600,7 +845,7 @@ extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const s
         hipLaunchKernelGGL((spt::k_sddmm<4, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
                            (int)ntiles, L.A.cap, part);
     SP_CHECK_LAUNCH();
-    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, st);
+    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, part + ntiles * L.A.cap, st);
 }
 
 extern "C" sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW, const int32_t *w_oc,

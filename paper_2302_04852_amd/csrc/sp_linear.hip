@@ -1,21 +1,14 @@
 // Sparse linear layers on gfx950 (SparseProp Sec. 3.2): structure
-// preparation -- encoders from a dense pattern, the CSC view and the tiled
-// plan -- and the three passes: forward product, input gradient (Eq. 1) and
-// weight gradient sampled at the stored entries (Eq. 2).  The compute work
-// runs in the tiled kernels of sp_tiled.h; this file supplies the linear
+// preparation -- encoders from a dense pattern, the CSC view and the
+// row-slot plan -- and the three passes: forward product, input gradient
+// (Eq. 1) and weight gradient sampled at the stored entries (Eq. 2).  The
+// compute work runs in the row-slot kernels of sp_spmm2.h; this file supplies the linear
 // geometry: tokens are rows of row-major [B][features] matrices.
 #include "sp_spmm2.h"
-#include "sp_tiled.h"
 
 namespace {
 
-using spt::C;
-using spt::NTHR;
-using spt::NW;
-using spt::PF;
-using spt::T;
-using spt::TS;
-
+constexpr int C = 64;  // column granularity of the fast staging mode
 constexpr int TR_BLK = 32;  // rows per block of the stable transpose
 
 // --------------------------------------------------------------------------
@@ -143,145 +136,16 @@ sp_status csc_build(int64_t in_f, int64_t out_f, const int32_t *row_ptr, const i
 }
 
 // --------------------------------------------------------------------------
-// Linear geometry.  G is In[ntok][ld] (only columns < ncols are read); the
-// SpMM output is Out[ntok][ldo]; the SDDMM stationary operand is D[ntok][ldd].
-// MODE 2 (fast): ld % 4 == 0, ncols % 64 == 0 and the operand spans < 2 GiB.
-//   Slabs are read with buffer loads whose per-thread offsets are fixed for
-//   the whole kernel and whose slab position is a scalar offset; the buffer
-//   range check returns zeros for rows past the last token.
+// Linear geometry of the row-slot kernels (sp_spmm2.h).  G is In[ntok][ld]
+// (columns < ncols), the output Out[ntok][ldo] (rows < nrows), the SDDMM
+// stationary operand D[ntok][ldd].  Staging: thread tid holds tokens
+// 4*(tid & 15) .. +3 and, in each part h of the chunk, columns
+// CW*h + 4*(tid >> 4) .. +3 (CW = 4 * threads / 16) -- 16-byte loads of four
+// token rows, written to LDS as 16-byte columns.
+// MODE 2 (fast): ld % 4 == 0, ncols % 64 == 0 and the operand spans < 2 GiB;
+//   buffer loads whose range check returns zeros past the last token.
 // MODE 1: ld % 4 == 0 otherwise; clamped 16-byte loads plus a validity mask.
 // MODE 0: general; clamped 4-byte loads plus a validity mask.
-template <int MODE>
-struct LinGeo {
-    const float *In;
-    int64_t ntok, ld, ncols;
-    float *Out;
-    int64_t ldo, nrows;
-    const float *D;
-    int64_t ldd;
-
-    struct Tok {
-        sp_i32x4 rsrc;
-        int voff;   // byte offset of this thread's first piece within a slab
-        int xsoff;  // float offset of this thread's first LDS element
-    };
-    // Slab pieces: 4096 float4, piece f = tid + NTHR*i; a wave instruction
-    // covers 16 tokens x 4 float4 (64-byte row segments) and the transposed
-    // LDS writes hit 64 distinct banks.  For thread (lane, wave w) and piece
-    // i: token t = (lane & 15) + 16w, float4 column qd = (lane >> 4) + 4i.
-    __device__ void tile_init(Tok &tk, int64_t t0, int lane) const {
-        const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-        const int t = (lane & 15) + 16 * w;
-        if (MODE == 2) {
-            const int64_t rows_left = ntok - t0;  // >= 1
-            tk.rsrc = sp::make_rsrc(In + t0 * ld, (uint32_t)(rows_left * ld * 4));
-            tk.voff = (int)((t * ld + 4 * (lane >> 4)) * 4);
-        }
-        tk.xsoff = 4 * (lane >> 4) * TS + t;
-    }
-    __device__ uint32_t load_slab(float (&pf)[PF], const Tok &tk, int64_t t0, int64_t c0, int tid) const {
-        if (MODE == 2) {
-            const int soff = (int)(c0 * 4);
-#pragma unroll
-            for (int i = 0; i < PF / 4; ++i) {
-                const sp_f32x4 v = sp_raw_buffer_load_f32x4(tk.rsrc, tk.voff + 64 * i, soff, 0);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) pf[4 * i + e] = v[e];
-            }
-            return 0xffffffffu;
-        }
-        const int lane = tid & 63, w = tid >> 6;
-        uint32_t mask = 0;
-#pragma unroll
-        for (int i = 0; i < PF / 4; ++i) {
-            const int t = (lane & 15) + 16 * w;
-            const int qd = (lane >> 4) + 4 * i;
-            const int64_t gt = t0 + t, gc = c0 + 4 * qd;
-            const int64_t ct = gt < ntok ? gt : ntok - 1;
-            if (MODE == 1) {
-                const int64_t cc = gc < ncols ? gc : ncols - 4;
-                const float4 v = *reinterpret_cast<const float4 *>(In + ct * ld + cc);
-                pf[4 * i + 0] = v.x;
-                pf[4 * i + 1] = v.y;
-                pf[4 * i + 2] = v.z;
-                pf[4 * i + 3] = v.w;
-                if (gt < ntok && gc < ncols) mask |= 0xfu << (4 * i);
-            } else {
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int64_t ge = gc + e;
-                    pf[4 * i + e] = In[ct * ld + (ge < ncols ? ge : ncols - 1)];
-                    if (gt < ntok && ge < ncols) mask |= 1u << (4 * i + e);
-                }
-            }
-        }
-        return mask;
-    }
-    __device__ void write_slab(float *xs, const float (&pf)[PF], uint32_t mask, const Tok &tk, int) const {
-        float *x = xs + tk.xsoff;
-#pragma unroll
-        for (int i = 0; i < PF / 4; ++i)
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                x[(16 * i + e) * TS] = (MODE == 2 || ((mask >> (4 * i + e)) & 1u)) ? pf[4 * i + e] : 0.f;
-    }
-
-    // Output tile through LDS (two halves of 128 tokens) so that global stores
-    // are full row segments of R floats.
-    template <int RW>
-    __device__ void store(float *ys, const float (&acc)[RW][4], const Tok &, int64_t t0, int64_t row0, int tid,
-                          int lane, int rw0) const {
-        constexpr int R = NW * RW, YS = R + 1;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            __syncthreads();
-            if ((lane >> 5) == h) {
-                const int tl = 4 * (lane & 31);
-#pragma unroll
-                for (int r = 0; r < RW; ++r)
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) ys[(tl + k) * YS + rw0 + r] = acc[r][k];
-            }
-            __syncthreads();
-            for (int e = tid; e < 128 * R; e += NTHR) {
-                const int tl = e / R, r = e % R;
-                const int64_t gt = t0 + 128 * h + tl, gr = row0 + r;
-                if (gt < ntok && gr < nrows) Out[gt * ldo + gr] = ys[tl * YS + r];
-            }
-        }
-    }
-
-    // D[t0 + 4*lane + k][row0 + rw0 + r] -> d[r][k], through LDS in two halves.
-    template <int RW>
-    __device__ void load_d(float *ys, float (&d)[RW][4], const Tok &, int64_t t0, int64_t row0, int tid, int lane,
-                           int rw0) const {
-        constexpr int R = NW * RW, YS = R + 1;
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            __syncthreads();
-            for (int e = tid; e < 128 * R; e += NTHR) {
-                const int tl = e / R, r = e % R;
-                const int64_t gt = t0 + 128 * h + tl, gr = row0 + r;
-                ys[tl * YS + r] = (gt < ntok && gr < nrows) ? D[gt * ldd + gr] : 0.f;
-            }
-            __syncthreads();
-            if ((lane >> 5) == h) {
-                const int tl = 4 * (lane & 31);
-#pragma unroll
-                for (int r = 0; r < RW; ++r)
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) d[r][k] = ys[(tl + k) * YS + rw0 + r];
-            }
-        }
-    }
-};
-
-// Linear geometry of the row-slot SpMM (sp_spmm2.h).  G is In[ntok][ld]
-// (columns < ncols), the output Out[ntok][ldo] (rows < nrows).  Staging:
-// thread tid holds tokens 4*(tid & 15) .. +3 and, in each part h of the
-// chunk, columns CW*h + 4*(tid >> 4) .. +3 (CW = 4 * threads / 16) -- 16-byte
-// loads of four token rows, written to LDS as 16-byte columns.  MODE as for
-// LinGeo.
 template <int MODE>
 struct LinGeo2 {
     const float *In;
@@ -413,8 +277,7 @@ struct LinGeo2 {
 // Plan layout: a pure function of (in_f, out_f, nnz).
 struct PlanLayout {
     int32_t *t_col_ptr, *t_row_idx, *t_perm;
-    spt::Tiling A;         // rows = out_f: weight gradient
-    spt2::SlotTiling F, G; // row slots: F rows = out_f (forward), G rows = in_f (input gradient)
+    spt2::SlotTiling F, G; // row slots: F rows = out_f (forward, weight gradient), G rows = in_f (input gradient)
     int32_t *cnt;          // scratch [max over the tilings of rows * chunks]
     int32_t *blk_cnt;   // transpose scratch [ceil(out_f/TR_BLK) * in_f]
     size_t bytes;
@@ -426,10 +289,9 @@ PlanLayout plan_layout(const void *base, int64_t in_f, int64_t out_f, int64_t nn
     L.t_col_ptr = c.take<int32_t>(in_f + 1);
     L.t_row_idx = c.take<int32_t>(nnz);
     L.t_perm = c.take<int32_t>(nnz);
-    spt::tiling_layout(c, L.A, out_f, in_f, nnz);
     spt2::slot_layout(c, L.F, out_f, in_f, nnz);
     spt2::slot_layout(c, L.G, in_f, out_f, nnz);
-    L.cnt = c.take<int32_t>(std::max(out_f * L.A.K, std::max(out_f * L.F.K, in_f * L.G.K)));
+    L.cnt = c.take<int32_t>(std::max(out_f * L.F.K, in_f * L.G.K));
     L.blk_cnt = c.take<int32_t>(sp::ceil_div(out_f, TR_BLK) * in_f);
     L.bytes = c.off;
     return L;
@@ -439,8 +301,6 @@ bool bad_dims(int64_t a, int64_t b, int64_t nnz) {
     return a < 0 || b < 0 || nnz < 0 || nnz > 0x7fffffffLL || a > 0x7fffffffLL || b > 0x7fffffffLL ||
            (a > 0 && b > 0 && nnz > a * b) || ((a == 0 || b == 0) && nnz > 0);
 }
-
-int64_t ntiles_of(int64_t ntok) { return sp::ceil_div(ntok, T); }
 
 // Staging mode of a [ntok][ncols] gathered operand (see LinGeo).
 int lin_mode(int64_t ntok, int64_t ncols) {
@@ -551,7 +411,6 @@ extern "C" sp_status sp_linear_plan(int64_t in_f, int64_t out_f, const int32_t *
     sp_status s;
     if ((s = csc_build(in_f, out_f, row_ptr, col_idx, nnz, L.t_col_ptr, L.t_row_idx, L.t_perm, L.blk_cnt, st)))
         return s;
-    if ((s = spt::tiling_build(L.A, row_ptr, col_idx, nullptr, L.cnt, st))) return s;
     if ((s = spt2::slot_build(L.F, row_ptr, col_idx, nullptr, L.cnt, st))) return s;
     return spt2::slot_build(L.G, L.t_col_ptr, L.t_row_idx, L.t_perm, L.cnt, st);
 }

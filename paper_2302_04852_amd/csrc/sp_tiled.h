@@ -86,9 +86,11 @@ inline void tiling_layout(sp::Carve &c, Tiling &t, int64_t rows, int64_t cols, i
 sp_status tiling_build(const Tiling &t, const int32_t *ptr, const int32_t *idx, const int32_t *src_map,
                        int32_t *cnt, hipStream_t st);
 
-// part[q][e] summed over q in a fixed order into grad[e_src[e]] (padding skipped).
+// part[q][e] summed over q in a fixed order into grad[e_src[e]] (padding
+// skipped).  part2: scratch of reduce_blocks(ntiles) * cap floats.
+int64_t reduce_blocks(int64_t ntiles);
 sp_status sddmm_reduce(const float *part, int64_t ntiles, int64_t cap, const int32_t *e_src, float *grad,
-                       hipStream_t st);
+                       float *part2, hipStream_t st);
 
 __device__ inline void fma4(float (&a)[4], float v, const float4 &x) {
     a[0] = fmaf(v, x.x, a[0]);

@@ -70,25 +70,35 @@ __global__ void k_fill_u16(uint16_t *p, int64_t n, uint16_t v) {
 // of 16 run sums, then the 256-tile block sums): every partial passes
 // through at most 32 + ntiles/256 additions, which keeps the fp32 rounding
 // bound small relative to the sum of absolute terms even for the longest
-// reductions (hundreds of thousands of pixels per weight).
-__global__ __launch_bounds__(256) void k_sddmm_reduce(const float *__restrict__ part, int64_t ntiles, int64_t cap,
-                                                      const int32_t *__restrict__ e_src, float *__restrict__ grad) {
+// reductions (hundreds of thousands of pixels per weight).  Two passes:
+// part2[g][e] = the sum of block g (256 tiles) of entry e, one thread per
+// (block, entry); then grad = the block sums added in block order.
+__global__ __launch_bounds__(256) void k_sddmm_reduce_blocks(const float *__restrict__ part, int64_t ntiles,
+                                                             int64_t cap, const int32_t *__restrict__ e_src,
+                                                             float *__restrict__ part2) {
+    const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t g = blockIdx.y;
+    if (e >= cap || e_src[e] < 0) return;
+    const int64_t q2 = g * 256, e2 = q2 + 256 < ntiles ? q2 + 256 : ntiles;
+    float s2 = 0.f;
+    for (int64_t q1 = q2; q1 < e2; q1 += 16) {
+        const int64_t e1 = q1 + 16 < e2 ? q1 + 16 : e2;
+        float s1 = 0.f;
+        for (int64_t q = q1; q < e1; ++q) s1 += part[q * cap + e];
+        s2 += s1;
+    }
+    part2[g * cap + e] = s2;
+}
+
+__global__ __launch_bounds__(256) void k_sddmm_reduce_final(const float *__restrict__ part2, int64_t nblk, int64_t cap,
+                                                            const int32_t *__restrict__ e_src,
+                                                            float *__restrict__ grad) {
     const int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (e >= cap) return;
     const int32_t s = e_src[e];
     if (s < 0) return;
     float acc = 0.f;
-    for (int64_t q2 = 0; q2 < ntiles; q2 += 256) {
-        const int64_t e2 = q2 + 256 < ntiles ? q2 + 256 : ntiles;
-        float s2 = 0.f;
-        for (int64_t q1 = q2; q1 < e2; q1 += 16) {
-            const int64_t e1 = q1 + 16 < e2 ? q1 + 16 : e2;
-            float s1 = 0.f;
-            for (int64_t q = q1; q < e1; ++q) s1 += part[q * cap + e];
-            s2 += s1;
-        }
-        acc += s2;
-    }
+    for (int64_t g = 0; g < nblk; ++g) acc += part2[g * cap + e];
     grad[s] = acc;
 }
 
@@ -124,11 +134,18 @@ sp_status tiling_build(const Tiling &t, const int32_t *ptr, const int32_t *idx, 
     return SP_OK;
 }
 
+int64_t reduce_blocks(int64_t ntiles) { return sp::ceil_div(ntiles, 256); }
+
 sp_status sddmm_reduce(const float *part, int64_t ntiles, int64_t cap, const int32_t *e_src, float *grad,
-                       hipStream_t st) {
-    if (cap <= 0) return SP_OK;
-    hipLaunchKernelGGL(k_sddmm_reduce, dim3((unsigned)sp::ceil_div(cap, 256)), dim3(256), 0, st, part, ntiles, cap,
-                       e_src, grad);
+                       float *part2, hipStream_t st) {
+    if (cap <= 0 || ntiles <= 0) return SP_OK;
+    const int64_t nblk = reduce_blocks(ntiles);
+    if (nblk > 65535) return SP_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(k_sddmm_reduce_blocks, dim3((unsigned)sp::ceil_div(cap, 256), (unsigned)nblk), dim3(256), 0,
+                       st, part, ntiles, cap, e_src, part2);
+    SP_CHECK_LAUNCH();
+    hipLaunchKernelGGL(k_sddmm_reduce_final, dim3((unsigned)sp::ceil_div(cap, 256)), dim3(256), 0, st, part2, nblk,
+                       cap, e_src, grad);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }

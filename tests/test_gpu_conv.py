@@ -206,6 +206,10 @@ SMALL = [
     (2, 6, 9, 9, 5, 3, 3, (1, 1), (1, 1), 0.0),          # dense
     (1, 2, 3, 3, 3, 3, 3, (1, 1), (0, 0), 0.0),          # 1x1 output
     (7, 9, 6, 5, 130, 2, 2, (1, 2), (0, 1), 0.6),        # 130 output channels, even kernel
+    (2, 12, 9, 11, 20, 3, 3, (2, 2), (0, 0), 0.6),       # stride 2, odd sizes, no padding: phase classes
+    (3, 20, 10, 7, 9, 2, 4, (2, 2), (1, 2), 0.5),        # stride 2, even kernel sizes
+    (2, 1, 15, 15, 8, 5, 5, (2, 2), (2, 2), 0.4),        # one input channel (direct kernel), stride 2
+    (2, 8, 6, 6, 300, 3, 3, (1, 1), (1, 1), 0.9),        # 8 input channels, 2700 columns (entry rounds)
 ]
 
 
@@ -261,21 +265,40 @@ def test_empty_pattern_and_empty_batch(sp, orc):
     assert torch.all(dW == 0)
 
 
-def test_plan_is_shape_independent(sp, orc):
-    """A plan depends on the pattern only: one plan serves two spatial sizes,
-    strides and batches."""
+@pytest.mark.parametrize("IC", [10, 3])
+def test_plan_is_shape_independent(sp, orc, IC):
+    """A plan depends on the pattern only: one plan serves other spatial
+    sizes, strides, paddings and batches, for all three passes (stride 2 in
+    both directions picks the tap class of each phase from the padding; with
+    IC <= 8 the direct input-gradient kernel serves)."""
     import torch
-    d, dims = _layer(orc, 7300, 2, 10, 12, 12, 14, 3, 3, (1, 1), (1, 1), 0.7)
+    d, dims = _layer(orc, 7300 + IC, 2, IC, 12, 12, 14, 3, 3, (1, 1), (1, 1), 0.7)
     L = GpuConv(sp, orc, d["mask"], d["W"], dims[0], dims[2], dims[3], dims[7], dims[8])
-    dims2 = (3, 10, 9, 11, 14, 3, 3, (2, 1), (0, 1))
-    s2 = sp.conv_shape(*dims2)
-    oh, ow = sp.sp_conv_out_hw(s2)
     rng = np.random.default_rng(3)
-    X = rng.standard_normal(dims2[:4]).astype(np.float32)
-    Y = torch.full((3, 14, oh, ow), float("nan"), device="cuda")
-    sp.sp_conv_fwd(torch.from_numpy(X).cuda(), s2, L.w_vals, L.nnz, L.plan, Y)
-    Yr, Ya = orc.conv_fwd(X, orc.conv_shape(*dims2), *L.o)
-    assert_parity(Y.cpu().numpy(), Yr, Ya, "second shape fwd")
+    for dims2 in [(3, IC, 9, 11, 14, 3, 3, (2, 1), (0, 1)), (2, IC, 13, 10, 14, 3, 3, (2, 2), (0, 1)),
+                  (2, IC, 11, 12, 14, 3, 3, (2, 2), (1, 0)), (1, IC, 8, 9, 14, 3, 3, (1, 1), (2, 0))]:
+        s2 = sp.conv_shape(*dims2)
+        os2 = orc.conv_shape(*dims2)
+        oh, ow = sp.sp_conv_out_hw(s2)
+        B2 = dims2[0]
+        X = rng.standard_normal(dims2[:4]).astype(np.float32)
+        dY = rng.standard_normal((B2, 14, oh, ow)).astype(np.float32)
+        Y = torch.full((B2, 14, oh, ow), float("nan"), device="cuda")
+        dX = torch.full(dims2[:4], float("nan"), device="cuda")
+        dW = torch.full((max(L.nnz, 1),), float("nan"), device="cuda")
+        ws = torch.empty(max(sp.sp_conv_bwd_weight_ws(s2, L.nnz), 1), dtype=torch.uint8, device="cuda")
+        Xd, dYd = torch.from_numpy(X).cuda(), torch.from_numpy(dY).cuda()
+        sp.sp_conv_fwd(Xd, s2, L.w_vals, L.nnz, L.plan, Y)
+        sp.sp_conv_bwd_input(dYd, s2, L.w_vals, L.nnz, L.plan, dX)
+        sp.sp_conv_bwd_weight(dYd, Xd, s2, L.nnz, L.plan, dW, ws)
+        torch.cuda.synchronize()
+        what = "shape %s" % (dims2,)
+        Yr, Ya = orc.conv_fwd(X, os2, *L.o)
+        assert_parity(Y.cpu().numpy(), Yr, Ya, what + " fwd")
+        dXr, dXa = orc.conv_bwd_input(dY, os2, *L.o)
+        assert_parity(dX.cpu().numpy(), dXr, dXa, what + " bwd_input")
+        dWr, dWa = orc.conv_bwd_weight(dY, X, os2, *L.o[:4])
+        assert_parity(dW.cpu().numpy()[:L.nnz], dWr, dWa, what + " bwd_weight")
 
 
 def test_deterministic(sp, orc):
