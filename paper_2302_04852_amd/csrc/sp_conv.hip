@@ -299,7 +299,7 @@ struct ConvGeo {
 
     template <int RW>
     __device__ void store(float *ys, const float (&acc)[RW][4], const Tok &tk, int64_t, int64_t row0, int tid,
-                          int lane, int rw0) const {
+                          int lane, int rw0, bool accumulate) const {
         constexpr int R = NW * RW;
         static_assert(R * YS <= spt::XS_FLOATS, "output staging exceeds the slab buffer");
 #pragma unroll
@@ -317,7 +317,12 @@ struct ConvGeo {
             if (ob >= 0) {
                 for (int r = tid >> 7; r < R; r += NTHR / 128) {
                     const int64_t gr = row0 + r;
-                    if (gr < orows) Out[ob + gr * onpix] = ys[r * YS + tl];
+                    if (gr < orows) {
+                        if (accumulate)
+                            unsafeAtomicAdd(Out + ob + gr * onpix, ys[r * YS + tl]);
+                        else
+                            Out[ob + gr * onpix] = ys[r * YS + tl];
+                    }
                 }
             }
         }
@@ -587,20 +592,40 @@ ConvGeo<1> phase_geo(const Dims &d, int a, int b, const TapClass &tc) {
     return g;
 }
 
+// Slab splits of an SpMM launch: two when the (panel, token tile) grid alone
+// leaves compute units without a workgroup; the partial outputs then meet in
+// the zero-filled output (see sp_tiled.h).  Above that the zero fill and the
+// atomic adds cost more than the extra parallelism gains (measured).
+constexpr int64_t NUM_CU = 256;
+int spmm_splits(const spt::Tiling &t, int64_t ntok) {
+    return (t.P * sp::ceil_div(ntok, T) < NUM_CU && t.K >= 2) ? 2 : 1;
+}
+
+// The output must hold zeros where nks == 2.
 template <class Geo>
-sp_status spmm(const spt::Tiling &t, const Geo &geo, const float *vals, hipStream_t st) {
+sp_status spmm(const spt::Tiling &t, const Geo &geo, const float *vals, int nks, hipStream_t st) {
     const int64_t ntiles = sp::ceil_div(geo.ntok, T);
-    const int64_t nwg = t.P * ntiles;
+    const int64_t nwg = t.P * ntiles * nks;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     if (nwg == 0) return SP_OK;
     if (t.R == 128)
         hipLaunchKernelGGL((spt::k_spmm<8, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
-                           (int)ntiles);
+                           (int)ntiles, nks);
     else
         hipLaunchKernelGGL((spt::k_spmm<4, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
-                           (int)ntiles);
+                           (int)ntiles, nks);
     SP_CHECK_LAUNCH();
     return SP_OK;
+}
+
+// Full SpMM of one output tensor: zero-fill first when the slabs are split.
+template <class Geo>
+sp_status spmm_full(const spt::Tiling &t, const Geo &geo, const float *vals, float *out, int64_t out_elems,
+                    hipStream_t st) {
+    const int nks = spmm_splits(t, geo.ntok);
+    sp_status r;
+    if (nks > 1 && (r = zero_launch(out, out_elems, st))) return r;
+    return spmm(t, geo, vals, nks, st);
 }
 
 // Direct input gradient for layers with at most FR_MAX input channels (image
@@ -647,7 +672,21 @@ __global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__
         for (int r = 0; r < FR_MAX; ++r) {
             if (r < nrows) {
                 const int j0 = max(ptr[r] - ptr[0] - e0, 0), j1 = min(ptr[r + 1] - ptr[0] - e0, ne);
-                for (int j = j0; j < j1; ++j) {
+                int j = j0;
+                for (; j + 8 <= j1; j += 8) {  // eight gathers in flight
+                    float x[8], v[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) {
+                        const int4 e = ent[j + u];
+                        const bool ok =
+                            (unsigned)(a - e.y) < (unsigned)g.gH && (unsigned)(c - e.z) < (unsigned)g.gW;
+                        x[u] = sp_raw_buffer_load_f32(rsrc, ok ? (gbase + e.x) * 4 : OOB, 0, 0);
+                        v[u] = __int_as_float(e.w);
+                    }
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) acc[r] = fmaf(v[u], x[u], acc[r]);
+                }
+                for (; j < j1; ++j) {
                     const int4 e = ent[j];
                     const bool ok = (unsigned)(a - e.y) < (unsigned)g.gH && (unsigned)(c - e.z) < (unsigned)g.gW;
                     const float x = sp_raw_buffer_load_f32(rsrc, ok ? (gbase + e.x) * 4 : OOB, 0, 0);
@@ -674,11 +713,12 @@ sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, c
 
 // Input gradient of one unit-stride problem (the whole layer at stride 1, or
 // one phase of a stride-2 layer) over a CSR by input channel and its tiling.
+// nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
 sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt::Tiling &t, const int32_t *ptr,
-                         const int32_t *col, const int32_t *src, const float *vals, hipStream_t st) {
+                         const int32_t *col, const int32_t *src, const float *vals, int nks, hipStream_t st) {
     if (g.ntok == 0) return SP_OK;
     if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, st);
-    return spmm(t, g, vals, st);
+    return spmm(t, g, vals, nks, st);
 }
 
 int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, T); }
@@ -768,7 +808,7 @@ extern "C" sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const f
     ConvGeo<0> g = make_geo<0>(d, true);
     g.G = X;
     g.Out = Y;
-    return spmm(L.A, g, w_vals, st);
+    return spmm_full(L.A, g, w_vals, Y, d.B * d.OC * d.OH * d.OW, st);
 }
 
 extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, const float *w_vals, int64_t nnz,
@@ -782,27 +822,38 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
     hipStream_t st = (hipStream_t)stream;
     if (nnz == 0) return zero_launch(dX, d.B * d.IC * d.H * d.W, st);
     ConvPlan L = plan_layout(plan, d, nnz);
+    const int64_t nout = d.B * d.IC * d.H * d.W;
     if (d.sh == 1 && d.sw == 1) {
         ConvGeo<1> g = make_geo<1>(d, false);
         g.G = dY;
         g.Out = dX;
-        return bwd_input_part(d, g, L.Bt, L.t_ic_ptr, L.colB, L.t_perm, w_vals, st);
+        const int nks = d.IC <= FR_MAX ? 1 : spmm_splits(L.Bt, g.ntok);
+        if (nks > 1 && (r = zero_launch(dX, nout, st))) return r;
+        return bwd_input_part(d, g, L.Bt, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nks, st);
     }
     if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
-        for (int a = 0; a < 2; ++a)
-            for (int b = 0; b < 2; ++b) {
-                const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
-                ConvGeo<1> g = phase_geo(d, a, b, cp.tc);
-                g.G = dY;
-                g.Out = dX;
-                if ((r = bwd_input_part(d, g, cp.T, cp.ptr, cp.col, cp.src, w_vals, st))) return r;
-            }
+        ConvGeo<1> g[4];
+        int nks[4], split = 0;
+        for (int ph = 0; ph < 4; ++ph) {
+            const int a = ph >> 1, b = ph & 1;
+            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
+            g[ph] = phase_geo(d, a, b, cp.tc);
+            g[ph].G = dY;
+            g[ph].Out = dX;
+            nks[ph] = d.IC <= FR_MAX ? 1 : spmm_splits(cp.T, g[ph].ntok);
+            split |= nks[ph] > 1;
+        }
+        if (split && (r = zero_launch(dX, nout, st))) return r;
+        for (int ph = 0; ph < 4; ++ph) {
+            const ClassPart &cp = L.cls[(((ph >> 1) + d.ph) & 1) * 2 + (((ph & 1) + d.pw) & 1)];
+            if ((r = bwd_input_part(d, g[ph], cp.T, cp.ptr, cp.col, cp.src, w_vals, nks[ph], st))) return r;
+        }
         return SP_OK;
     }
     ConvGeo<2> g = make_geo<2>(d, false);
     g.G = dY;
     g.Out = dX;
-    return spmm(L.Bt, g, w_vals, st);
+    return spmm_full(L.Bt, g, w_vals, dX, nout, st);
 }
 
 extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes) {
@@ -832,7 +883,11 @@ extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const s
     if (d.B == 0) return zero_launch(dW, nnz, st);
     ConvPlan L = plan_layout(plan, d, nnz);
     const int64_t ntiles = wgrad_tiles(d);
-    const int64_t nwg = L.A.P * ntiles;
+    // Slab splits: enough workgroups for four per compute unit where the
+    // (panel, token tile) grid alone is smaller.
+    const int nks = (int)std::max<int64_t>(
+        1, std::min<int64_t>(L.A.K, sp::ceil_div(4 * NUM_CU, std::max<int64_t>(L.A.P * ntiles, 1))));
+    const int64_t nwg = L.A.P * ntiles * nks;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     ConvGeo<0> g = make_geo<0>(d, true);
     g.G = X;
@@ -840,10 +895,10 @@ extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const s
     float *part = (float *)workspace;
     if (L.A.R == 128)
         hipLaunchKernelGGL((spt::k_sddmm<8, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
-                           (int)ntiles, L.A.cap, part);
+                           (int)ntiles, nks, L.A.cap, part);
     else
         hipLaunchKernelGGL((spt::k_sddmm<4, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
-                           (int)ntiles, L.A.cap, part);
+                           (int)ntiles, nks, L.A.cap, part);
     SP_CHECK_LAUNCH();
     return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, part + ntiles * L.A.cap, st);
 }

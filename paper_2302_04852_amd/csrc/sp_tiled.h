@@ -9,7 +9,12 @@
 // tap (implicit im2col), so no unfolded matrix is ever written.
 //
 // Work decomposition.  A workgroup of 16 waves owns 256 tokens x R = 16*RW
-// rows (RW = 8 or 4 rows per wave).  Lanes map to tokens, 4 consecutive
+// rows (RW = 8 or 4 rows per wave) and a range of the slabs: small layers
+// split the slabs over nks workgroups so that enough of them exist to fill
+// the chip.  The SpMM then accumulates its partial outputs into the
+// zero-filled output with atomic adds (with nks = 2 the result does not
+// depend on their order: 0 + a + b = 0 + b + a exactly); the SDDMM needs no
+// combination, since every entry belongs to exactly one slab.  Lanes map to tokens, 4 consecutive
 // tokens per lane; wave w owns rows [RW*w, RW*w + RW).  G is staged one slab of 64 columns at a time
 // into LDS as xs[column][token] (stride TS), so one lane's 4 tokens are one
 // 16-byte LDS read; an extra all-zero column backs the padding entries.  The
@@ -146,14 +151,16 @@ struct MetaPF {
 // address) and validity is applied when the registers are written to LDS,
 // so the compute never waits on the prefetch.
 template <int RW, class Geo>
-__global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict__ vals, TileView tv, int ntiles) {
+__global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict__ vals, TileView tv, int ntiles,
+                                               int nks) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
     __shared__ __attribute__((aligned(16))) float4 meta4[CAP / 2 + 2];
     float2 *meta = reinterpret_cast<float2 *>(meta4);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles);
-    const int p = L % tv.P, q = L / tv.P;
+    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks);
+    const int p = L % tv.P, q = (L / tv.P) % ntiles, ks = L / (tv.P * ntiles);
+    const int k0 = (int)((int64_t)ks * tv.K / nks), k1 = (int)((int64_t)(ks + 1) * tv.K / nks);
     const int64_t t0 = (int64_t)q * T;
     const int64_t row0 = (int64_t)p * tv.R;
     const int rw0 = wave * RW;
@@ -173,29 +180,29 @@ __global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict_
     float pf[PF];
     uint32_t pfm = 0;
     MetaPF m1{0, 0, false};
-    if (K > 0) {
-        const int32_t b0 = tv.pk_base[pk0];
-        const int n0 = min(tv.pk_base[pk0 + 1] - b0, CAP);
+    if (k1 > k0) {
+        const int32_t b0 = tv.pk_base[pk0 + k0];
+        const int n0 = min(tv.pk_base[pk0 + k0 + 1] - b0, CAP);
         for (int e = tid; e < n0; e += NTHR) {
             const int s = tv.e_src[b0 + e];
             meta[e] = make_float2(__int_as_float(s >= 0 ? (int)tv.e_col[b0 + e] * (TS * 4) : ZERO_OFF),
                                   s >= 0 ? vals[s] : 0.f);
         }
-        pfm = geo.load_slab(pf, tok, t0, 0, tid);
+        pfm = geo.load_slab(pf, tok, t0, (int64_t)k0 * C, tid);
         geo.write_slab(xs, pf, pfm, tok, tid);
-        m1.load(tv, pk0, min(1, K - 1), K > 1, tid);
+        m1.load(tv, pk0, min(k0 + 1, k1 - 1), k0 + 1 < k1, tid);
     }
     __syncthreads();
 
     const char *xb = reinterpret_cast<const char *>(xs) + lane * 16;
-    for (int k = 0; k < K; ++k) {
+    for (int k = k0; k < k1; ++k) {
         const int64_t pk = pk0 + k;
         const int32_t base = tv.pk_base[pk];
         const int cnt = tv.pk_base[pk + 1] - base;
         const float v1 = vals[m1.src > 0 ? m1.src : 0];
-        pfm = geo.load_slab(pf, tok, t0, (int64_t)min(k + 1, K - 1) * C, tid);
+        pfm = geo.load_slab(pf, tok, t0, (int64_t)min(k + 1, k1 - 1) * C, tid);
         MetaPF m2;
-        m2.load(tv, pk0, min(k + 2, K - 1), k + 2 < K, tid);
+        m2.load(tv, pk0, min(k + 2, k1 - 1), k + 2 < k1, tid);
 
         int ro[RW + 1];
 #pragma unroll
@@ -238,7 +245,7 @@ __global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict_
             }
         }
         __syncthreads();
-        if (k + 1 < K) {
+        if (k + 1 < k1) {
             geo.write_slab(xs, pf, pfm, tok, tid);
             const bool on = m1.ok && m1.src >= 0;
             meta[tid] = make_float2(__int_as_float(on ? m1.col * (TS * 4) : ZERO_OFF), on ? v1 : 0.f);
@@ -246,7 +253,7 @@ __global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict_
         m1 = m2;
         __syncthreads();
     }
-    geo.template store<RW>(xs, acc, tok, t0, row0, tid, lane, rw0);
+    geo.template store<RW>(xs, acc, tok, t0, row0, tid, lane, rw0, nks > 1);
 }
 
 // --------------------------------------------------------------------------
@@ -257,7 +264,7 @@ __global__ __launch_bounds__(NTHR) void k_spmm(Geo geo, const float *__restrict_
 // row with 16-byte reads, two lane swaps finish the sums) and lanes 0..15
 // write the 16 results.  Padding entries produce unused partials.
 template <int RW, class Geo>
-__global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles, int64_t cap,
+__global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles, int nks, int64_t cap,
                                                 float *__restrict__ part) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
     __shared__ __attribute__((aligned(16))) int2 meta2[CAP / 2 + 2];
@@ -265,8 +272,9 @@ __global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles
     int *meta = reinterpret_cast<int *>(meta2);
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles);
-    const int p = L % tv.P, q = L / tv.P;
+    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks);
+    const int p = L % tv.P, q = (L / tv.P) % ntiles, ks = L / (tv.P * ntiles);
+    const int k0 = (int)((int64_t)ks * tv.K / nks), k1 = (int)((int64_t)(ks + 1) * tv.K / nks);
     const int64_t t0 = (int64_t)q * T;
     const int64_t row0 = (int64_t)p * tv.R;
     const int rw0 = wave * RW;
@@ -286,13 +294,13 @@ __global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles
     float pf[PF];
     uint32_t pfm = 0;
     MetaPF m1{0, 0, false};
-    if (K > 0) {
-        const int32_t b0 = tv.pk_base[pk0];
-        const int n0 = min(tv.pk_base[pk0 + 1] - b0, CAP);
+    if (k1 > k0) {
+        const int32_t b0 = tv.pk_base[pk0 + k0];
+        const int n0 = min(tv.pk_base[pk0 + k0 + 1] - b0, CAP);
         for (int e = tid; e < n0; e += NTHR) meta[e] = (int)tv.e_col[b0 + e] * (TS * 4);
-        pfm = geo.load_slab(pf, tok, t0, 0, tid);
+        pfm = geo.load_slab(pf, tok, t0, (int64_t)k0 * C, tid);
         geo.write_slab(xs, pf, pfm, tok, tid);
-        m1.load(tv, pk0, min(1, K - 1), K > 1, tid);
+        m1.load(tv, pk0, min(k0 + 1, k1 - 1), k0 + 1 < k1, tid);
     }
     __syncthreads();
 
@@ -313,13 +321,13 @@ __global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles
         if (lane < n) pq[e0 + lane] = v;
     };
 
-    for (int k = 0; k < K; ++k) {
+    for (int k = k0; k < k1; ++k) {
         const int64_t pk = pk0 + k;
         const int32_t base = tv.pk_base[pk];
         const int cnt = tv.pk_base[pk + 1] - base;
-        pfm = geo.load_slab(pf, tok, t0, (int64_t)min(k + 1, K - 1) * C, tid);
+        pfm = geo.load_slab(pf, tok, t0, (int64_t)min(k + 1, k1 - 1) * C, tid);
         MetaPF m2;
-        m2.load(tv, pk0, min(k + 2, K - 1), k + 2 < K, tid);
+        m2.load(tv, pk0, min(k + 2, k1 - 1), k + 2 < k1, tid);
 
         int ro[RW + 1];
 #pragma unroll
@@ -367,7 +375,7 @@ __global__ __launch_bounds__(NTHR) void k_sddmm(Geo geo, TileView tv, int ntiles
             if (slot > 0) flush(slot, e0);
         }
         __syncthreads();
-        if (k + 1 < K) {
+        if (k + 1 < k1) {
             geo.write_slab(xs, pf, pfm, tok, tid);
             meta[tid] = m1.ok ? m1.col * (TS * 4) : ZERO_OFF;
         }
