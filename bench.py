@@ -380,8 +380,8 @@ CONV_DESC = {
     "resnet18": "ResNet-18 sparse layers at batch 64, 224x224, 95%: the 20 convolutions and the FC 512->1000; "
                 "fwd, bwd_input, bwd_weight of every layer (BN/ReLU/pooling not included)",
 }
-CONV_KERNEL = {"fwd": "k_spmm<ConvGeo<0>>", "bwd_input": "k_spmm<ConvGeo<1|2>>",
-               "bwd_weight": "k_sddmm<ConvGeo<0>>+k_sddmm_reduce"}
+CONV_KERNEL = {"fwd": "k_spmm2<ConvGeo<0>>", "bwd_input": "k_spmm2<ConvGeo<1|2>> / k_fewrows",
+               "bwd_weight": "k_sddmm2<ConvGeo<0>>+k_slot_reduce"}
 
 
 def run_conv(args, sp, torch, which):

@@ -1,10 +1,10 @@
 // Sparse convolutions on gfx950 (SparseProp Sec. 3.3): encoders of the
-// five-array format, its input-channel-major view, the tiled plan, and the
+// five-array format, its input-channel-major view, the row-slot plan, and the
 // three passes -- forward (Eq. 3), input gradient (Eq. 4) and weight gradient
 // at the stored entries (Eq. 5) -- with stride and zero padding.
 //
-// Each pass is one of the two tiled products of sp_tiled.h over an implicit
-// im2col operand.  A column of that operand is a (channel, tap) pair
+// Each pass is one of the two row-slot products of sp_spmm2.h over an
+// implicit im2col operand.  A column of that operand is a (channel, tap) pair
 // col = ch*KH*KW + x*KW + y, a token is one pixel of one image:
 //   forward, weight gradient: rows = output channels, columns = (ic, tap),
 //     tokens = output pixels (b, p, q), G[t][col] = X[b, ic, p*sh+x-ph, q*sw+y-pw];
@@ -20,27 +20,19 @@
 //     tap that cannot contribute.  Other strides use the general gather with
 //     the divisibility test.
 //     Layers with at most 8 input channels (image stems) use a direct kernel
-//     instead: a 16-wave tile would leave most waves without rows.
+//     instead: a 256-row tile would leave all but one wave without rows.
 // Within a row (channel) the format's (channel, x, y) order is exactly the
 // ascending column order, so the format itself is the CSR of the forward
 // tiling.  The gather uses raw buffer loads: an element outside the image
 // (zero padding), past the last token or past the last column gets an
 // offset beyond the buffer's range and loads as 0, so staging has no
 // branches.  This requires every activation tensor to span less than 2 GiB.
-#include "sp_tiled.h"
+#include "sp_spmm2.h"
 
 namespace {
 
-using spt::C;
-using spt::NTHR;
-using spt::NW;
-using spt::PF;
-using spt::T;
-using spt::TS;
-
 constexpr int OOB = 0x7ffffff0;       // byte offset beyond any accepted buffer range
 constexpr int TOK_INVALID = -(1 << 28);  // spatial origin of tokens past the end
-constexpr int YS = 132;               // LDS stride (floats) of one row of 128 tokens
 constexpr int64_t MAX_BYTES = 0x7fff0000LL;
 
 // --------------------------------------------------------------------------
@@ -188,16 +180,19 @@ sp_status zero_launch(float *p, int64_t n, hipStream_t st) {
 }
 
 // --------------------------------------------------------------------------
-// Convolution geometry for the tiled kernels.
+// Convolution geometry for the row-slot kernels (sp_spmm2.h).
 //   DIR 0: gather X by output pixels (forward, weight gradient);
-//   DIR 1: gather dY by input pixels, unit stride (input gradient);
+//   DIR 1: gather dY by input pixels, unit stride (input gradient; also one
+//          phase of a stride-2 input gradient);
 //   DIR 2: gather dY by input pixels, any stride (input gradient).
-// Staging: thread tid holds token tid & 255 of the tile and the 16
-// consecutive columns 16*(tid >> 8) .. +15 of the slab, so a wave
-// instruction loads one column for 64 consecutive pixels and the column's
-// (channel, x, y) is wave-uniform.  Output and the stationary operand of the
-// weight gradient go through LDS (two halves of 128 tokens) so that global
-// accesses are runs of consecutive pixels of one channel.
+// Staging: thread tid holds token tid & 63 of the 64-token tile and the 32
+// consecutive columns 32*w .. +31 of the chunk, w = tid >> 6 its wave, so a
+// wave instruction loads one column for 64 consecutive pixels and the
+// column's (channel, x, y) is wave-uniform.  Elements in the zero padding,
+// tokens past the end and columns past the last get an offset beyond the
+// buffer range and load as 0: staging has no branches.  Outputs and the
+// weight gradient's stationary operand are NCHW, read and written as runs of
+// consecutive pixels of one channel.
 template <int DIR>
 struct ConvGeo {
     const float *G;   // gathered tensor
@@ -215,54 +210,46 @@ struct ConvGeo {
     // (the identity map for the full pixel grid; a strided sub-grid for a phase).
     int onpix, oW, osh, osw, oa, ob;
 
+    static constexpr int CPW = spt2::KC / spt2::NW;  // columns staged per wave
+    static_assert(CPW == spt2::PF, "one token and CPW columns per thread");
+
     struct Tok {
-        int a, c;      // spatial origin of the staging token (see tile_init)
-        int gbase;     // element offset of that origin in G
-        int obase[2];  // element offset of the output pixels (tid & 127) + 128h, -1 if past the end
+        int a, c;   // spatial origin of the token (see tile_init)
+        int gbase;  // element offset of that origin in G
+        int obase;  // element offset of the token's output pixel in channel 0, -1 past the end
     };
 
-    __device__ void tile_init(Tok &tk, int64_t t0, int) const {
-        const int tid = threadIdx.x;
-        const int tg = (int)t0 + (tid & 255);
+    __device__ void tile_init(Tok &tk, int64_t t0) const {
+        const int t = (int)t0 + (int)(threadIdx.x & 63);
         tk.a = TOK_INVALID;
         tk.c = TOK_INVALID;
         tk.gbase = 0;
-        if (tg < ntok) {
-            const int b = tg / npix, pix = tg - b * npix;
-            const int r = pix / tw, s = pix - r * tw;
+        tk.obase = -1;
+        if (t < ntok) {
+            const int b = t / npix, pix = t - b * npix;
+            const int r = pix / tw, q = pix - r * tw;
             if (DIR == 0) {
                 tk.a = r * sh - ph;
-                tk.c = s * sw - pw;
+                tk.c = q * sw - pw;
                 tk.gbase = b * gimg + tk.a * gW + tk.c;
             } else {
                 tk.a = r + ph;
-                tk.c = s + pw;
+                tk.c = q + pw;
                 tk.gbase = DIR == 1 ? b * gimg + tk.a * gW + tk.c : b * gimg;
             }
-        }
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int ts = (int)t0 + (tid & 127) + 128 * h;
-            int o = -1;
-            if (ts < ntok) {
-                const int b = ts / npix, pix = ts - b * npix;
-                const int r = pix / tw, c = pix - r * tw;
-                o = b * orows * onpix + (r * osh + oa) * oW + c * osw + ob;
-            }
-            tk.obase[h] = o;
+            tk.obase = b * orows * onpix + (r * osh + oa) * oW + q * osw + ob;
         }
     }
 
-    __device__ uint32_t load_slab(float (&pf)[PF], const Tok &tk, int64_t, int64_t c0, int tid) const {
-        static_assert(PF == 16, "conv staging assumes 16 columns per thread");
+    __device__ uint32_t load_chunk(float (&pf)[spt2::PF], const Tok &tk, int64_t c0) const {
         const sp_i32x4 rsrc = sp::make_rsrc(G, (uint32_t)gbytes);
-        const int cb = (int)c0 + 16 * __builtin_amdgcn_readfirstlane(tid >> 8);
+        const int cb = (int)c0 + CPW * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
         int ch = cb / KK;
         const int tap = cb - ch * KK;
         int x = tap / KW;
         int y = tap - x * KW;
 #pragma unroll
-        for (int i = 0; i < PF; ++i) {
+        for (int i = 0; i < CPW; ++i) {
             const bool col_ok = cb + i < ncols;
             bool ok;
             int off;
@@ -291,69 +278,51 @@ struct ConvGeo {
         return 0xffffffffu;
     }
 
-    __device__ void write_slab(float *xs, const float (&pf)[PF], uint32_t, const Tok &, int tid) const {
-        float *x = xs + (tid >> 8) * 16 * TS + (tid & 255);
+    __device__ void write_chunk(float *xs, const float (&pf)[spt2::PF], uint32_t, const Tok &) const {
+        float *x = xs + (threadIdx.x >> 6) * CPW * spt2::T + (threadIdx.x & 63);
 #pragma unroll
-        for (int i = 0; i < PF; ++i) x[i * TS] = pf[i];
+        for (int i = 0; i < CPW; ++i) x[i * spt2::T] = pf[i];
     }
 
-    template <int RW>
-    __device__ void store(float *ys, const float (&acc)[RW][4], const Tok &tk, int64_t, int64_t row0, int tid,
-                          int lane, int rw0, bool accumulate) const {
-        constexpr int R = NW * RW;
-        static_assert(R * YS <= spt::XS_FLOATS, "output staging exceeds the slab buffer");
+    // Accumulators -> output through LDS: ys[position][64 tokens], then thread
+    // tid writes token tid & 63 of rows (tid >> 6) + 8j: runs of consecutive
+    // pixels of one channel.
+    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &tk, int64_t, int64_t row0,
+                          bool add) const {
+        const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
+        __syncthreads();
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            __syncthreads();
-            if ((lane >> 5) == h) {
-                const int tl = 4 * (lane & 31);
+        for (int s = 0; s < spt2::NS; ++s) {
+            const int pos = spt2::NG * spt2::NW * s + spt2::NG * w + g;
 #pragma unroll
-                for (int r = 0; r < RW; ++r)
-                    *reinterpret_cast<float4 *>(ys + (rw0 + r) * YS + tl) =
-                        make_float4(acc[r][0], acc[r][1], acc[r][2], acc[r][3]);
-            }
-            __syncthreads();
-            const int ob = tk.obase[h], tl = tid & 127;
-            if (ob >= 0) {
-                for (int r = tid >> 7; r < R; r += NTHR / 128) {
-                    const int64_t gr = row0 + r;
-                    if (gr < orows) {
-                        if (accumulate)
-                            unsafeAtomicAdd(Out + ob + gr * onpix, ys[r * YS + tl]);
-                        else
-                            Out[ob + gr * onpix] = ys[r * YS + tl];
-                    }
-                }
-            }
+            for (int k = 0; k < 4; ++k) ys[pos * spt2::YS + 4 * gl + k] = acc[s][k];
+        }
+        __syncthreads();
+        if (tk.obase < 0) return;
+        const int nr = (int)min<int64_t>(spt2::R, orows - row0);
+        for (int r = w; r < nr; r += spt2::NW) {
+            float *o = Out + tk.obase + (row0 + r) * onpix;
+            const float v = ys[r * spt2::YS + lane];
+            if (add)
+                unsafeAtomicAdd(o, v);
+            else
+                *o = v;
         }
     }
 
-    template <int RW>
-    __device__ void load_d(float *ys, float (&d)[RW][4], const Tok &tk, int64_t, int64_t row0, int tid, int lane,
-                           int rw0) const {
-        constexpr int R = NW * RW;
-        static_assert(R * YS <= spt::XS_FLOATS, "operand staging exceeds the slab buffer");
+    // D[token t0 + lane][rows of slot s of groups 0..3 of this wave], zero past
+    // the last token or row.
+    __device__ float4 load_dq(const Tok &tk, int64_t, int64_t row0, int s) const {
+        const int w = threadIdx.x >> 6;
+        const int64_t r = row0 + spt2::NG * spt2::NW * s + spt2::NG * w;
+        float v[4];
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            __syncthreads();
-            const int ob = tk.obase[h], tl = tid & 127;
-            for (int r = tid >> 7; r < R; r += NTHR / 128) {
-                const int64_t gr = row0 + r;
-                ys[r * YS + tl] = (ob >= 0 && gr < orows) ? D[ob + gr * onpix] : 0.f;
-            }
-            __syncthreads();
-            if ((lane >> 5) == h) {
-                const int tl4 = 4 * (lane & 31);
-#pragma unroll
-                for (int r = 0; r < RW; ++r) {
-                    const float4 v = *reinterpret_cast<const float4 *>(ys + (rw0 + r) * YS + tl4);
-                    d[r][0] = v.x;
-                    d[r][1] = v.y;
-                    d[r][2] = v.z;
-                    d[r][3] = v.w;
-                }
-            }
+        for (int g = 0; g < 4; ++g) {
+            const bool ok = tk.obase >= 0 && r + g < orows;
+            const float u = D[ok ? tk.obase + (r + g) * onpix : 0];
+            v[g] = ok ? u : 0.f;
         }
+        return make_float4(v[0], v[1], v[2], v[3]);
     }
 };
 
@@ -410,19 +379,19 @@ inline TapClass tap_class(int c, int KH, int KW) {
 
 // Per tap class of a stride-2 input gradient: the class's entries as a CSR
 // over input channels (columns (oc, i, j) ascending, value index in src) and
-// its tiling.  Sized for up to nnz entries each, since the split of the
-// entries between the classes is known only on the device.
+// its row-slot tiling.  Sized for up to nnz entries each, since the split of
+// the entries between the classes is known only on the device.
 struct ClassPart {
     TapClass tc;
     int32_t *ptr, *col, *src;
-    spt::Tiling T;
+    spt2::SlotTiling T;
 };
 
 struct ConvPlan {
     int32_t *t_ic_ptr, *t_oc, *t_perm;
     int32_t *colA, *colB;
-    spt::Tiling A, Bt;  // A: rows = OC, columns (ic, tap); Bt: rows = IC, columns (oc, tap)
-    ClassPart cls[4];   // stride-2 input gradient, one per tap class
+    spt2::SlotTiling F, G;  // F: rows = OC, columns (ic, tap); G: rows = IC, columns (oc, tap)
+    ClassPart cls[4];       // stride-2 input gradient, one per tap class
     int32_t *cnt;
     size_t bytes;
 };
@@ -437,17 +406,17 @@ ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
     L.t_perm = c.take<int32_t>(nnz);
     L.colA = c.take<int32_t>(nnz);
     L.colB = c.take<int32_t>(nnz);
-    spt::tiling_layout(c, L.A, d.OC, d.IC * d.KK, nnz);
-    spt::tiling_layout(c, L.Bt, d.IC, d.OC * d.KK, nnz);
+    spt2::slot_layout(c, L.F, d.OC, d.IC * d.KK, nnz);
+    spt2::slot_layout(c, L.G, d.IC, d.OC * d.KK, nnz);
     for (int k = 0; k < 4; ++k) {
         ClassPart &cp = L.cls[k];
         cp.tc = tap_class(k, d.KH, d.KW);
         cp.ptr = c.take<int32_t>(d.IC + 1);
         cp.col = c.take<int32_t>(nnz);
         cp.src = c.take<int32_t>(nnz);
-        spt::tiling_layout(c, cp.T, d.IC, d.OC * cp.tc.ncx * cp.tc.ncy, nnz);
+        spt2::slot_layout(c, cp.T, d.IC, d.OC * cp.tc.ncx * cp.tc.ncy, nnz);
     }
-    L.cnt = c.take<int32_t>(std::max(d.OC * L.A.K, d.IC * L.Bt.K));
+    L.cnt = c.take<int32_t>(std::max(d.OC * L.F.K, d.IC * L.G.K));
     L.bytes = c.off;
     return L;
 }
@@ -522,7 +491,7 @@ sp_status classes_build(const ConvPlan &L, const Dims &d, const uint8_t *w_x, co
         SP_CHECK_LAUNCH();
     }
     for (int k = 0; k < 4; ++k)
-        if ((r = spt::tiling_build(L.cls[k].T, L.cls[k].ptr, L.cls[k].col, L.cls[k].src, L.cnt, st))) return r;
+        if ((r = spt2::slot_build(L.cls[k].T, L.cls[k].ptr, L.cls[k].col, L.cls[k].src, L.cnt, st))) return r;
     return SP_OK;
 }
 
@@ -592,35 +561,30 @@ ConvGeo<1> phase_geo(const Dims &d, int a, int b, const TapClass &tc) {
     return g;
 }
 
-// Slab splits of an SpMM launch: two when the (panel, token tile) grid alone
+// Chunk splits of an SpMM launch: two when the (panel, token tile) grid alone
 // leaves compute units without a workgroup; the partial outputs then meet in
-// the zero-filled output (see sp_tiled.h).  Above that the zero fill and the
-// atomic adds cost more than the extra parallelism gains (measured).
+// the zero-filled output (see sp_spmm2.h).
 constexpr int64_t NUM_CU = 256;
-int spmm_splits(const spt::Tiling &t, int64_t ntok) {
-    return (t.P * sp::ceil_div(ntok, T) < NUM_CU && t.K >= 2) ? 2 : 1;
+int spmm_splits(const spt2::SlotTiling &t, int64_t ntok) {
+    return (t.P * sp::ceil_div(ntok, spt2::T) < NUM_CU && t.K >= 2) ? 2 : 1;
 }
 
 // The output must hold zeros where nks == 2.
 template <class Geo>
-sp_status spmm(const spt::Tiling &t, const Geo &geo, const float *vals, int nks, hipStream_t st) {
-    const int64_t ntiles = sp::ceil_div(geo.ntok, T);
+sp_status spmm(const spt2::SlotTiling &t, const Geo &geo, const float *vals, int nks, hipStream_t st) {
+    const int64_t ntiles = sp::ceil_div(geo.ntok, spt2::T);
     const int64_t nwg = t.P * ntiles * nks;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     if (nwg == 0) return SP_OK;
-    if (t.R == 128)
-        hipLaunchKernelGGL((spt::k_spmm<8, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
-                           (int)ntiles, nks);
-    else
-        hipLaunchKernelGGL((spt::k_spmm<4, Geo>), dim3((unsigned)nwg), dim3(NTHR), 0, st, geo, vals, t.view(),
-                           (int)ntiles, nks);
+    hipLaunchKernelGGL((spt2::k_spmm2<Geo>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals, t.view(),
+                       (int)ntiles, nks);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
 
-// Full SpMM of one output tensor: zero-fill first when the slabs are split.
+// Full SpMM of one output tensor: zero-fill first when the chunks are split.
 template <class Geo>
-sp_status spmm_full(const spt::Tiling &t, const Geo &geo, const float *vals, float *out, int64_t out_elems,
+sp_status spmm_full(const spt2::SlotTiling &t, const Geo &geo, const float *vals, float *out, int64_t out_elems,
                     hipStream_t st) {
     const int nks = spmm_splits(t, geo.ntok);
     sp_status r;
@@ -633,7 +597,7 @@ sp_status spmm_full(const spt::Tiling &t, const Geo &geo, const float *vals, flo
 // channel.  The channels' entries -- gather offset within dY, taps and value
 // -- are staged in LDS and read as wave-uniform broadcasts; dY is read
 // straight from global memory, neighbouring threads reading neighbouring
-// pixels.  A 16-wave tile would leave all but one wave without rows here.
+// pixels.  A 256-row tile would leave all but one wave without rows here.
 constexpr int FR_MAX = 8;
 constexpr int FR_ENT = 2048;  // entries staged per round (32 KB)
 
@@ -714,14 +678,14 @@ sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, c
 // Input gradient of one unit-stride problem (the whole layer at stride 1, or
 // one phase of a stride-2 layer) over a CSR by input channel and its tiling.
 // nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
-sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt::Tiling &t, const int32_t *ptr,
+sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,
                          const int32_t *col, const int32_t *src, const float *vals, int nks, hipStream_t st) {
     if (g.ntok == 0) return SP_OK;
     if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, st);
     return spmm(t, g, vals, nks, st);
 }
 
-int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, T); }
+int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, spt2::T); }
 
 }  // namespace
 
@@ -789,8 +753,8 @@ extern "C" sp_status sp_conv_plan(const sp_conv_shape *s, const int32_t *w_oc, c
                            w_y, nnz, d.KW, d.KK, L.colB);
         SP_CHECK_LAUNCH();
     }
-    if ((r = spt::tiling_build(L.A, w_oc, L.colA, nullptr, L.cnt, st))) return r;
-    if ((r = spt::tiling_build(L.Bt, L.t_ic_ptr, L.colB, L.t_perm, L.cnt, st))) return r;
+    if ((r = spt2::slot_build(L.F, w_oc, L.colA, nullptr, L.cnt, st))) return r;
+    if ((r = spt2::slot_build(L.G, L.t_ic_ptr, L.colB, L.t_perm, L.cnt, st))) return r;
     return classes_build(L, d, w_x, w_y, nnz, st);
 }
 
@@ -808,7 +772,7 @@ extern "C" sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const f
     ConvGeo<0> g = make_geo<0>(d, true);
     g.G = X;
     g.Out = Y;
-    return spmm_full(L.A, g, w_vals, Y, d.B * d.OC * d.OH * d.OW, st);
+    return spmm_full(L.F, g, w_vals, Y, d.B * d.OC * d.OH * d.OW, st);
 }
 
 extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, const float *w_vals, int64_t nnz,
@@ -827,9 +791,9 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         ConvGeo<1> g = make_geo<1>(d, false);
         g.G = dY;
         g.Out = dX;
-        const int nks = d.IC <= FR_MAX ? 1 : spmm_splits(L.Bt, g.ntok);
+        const int nks = d.IC <= FR_MAX ? 1 : spmm_splits(L.G, g.ntok);
         if (nks > 1 && (r = zero_launch(dX, nout, st))) return r;
-        return bwd_input_part(d, g, L.Bt, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nks, st);
+        return bwd_input_part(d, g, L.G, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nks, st);
     }
     if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
         ConvGeo<1> g[4];
@@ -853,7 +817,7 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
     ConvGeo<2> g = make_geo<2>(d, false);
     g.G = dY;
     g.Out = dX;
-    return spmm_full(L.Bt, g, w_vals, dX, nout, st);
+    return spmm_full(L.G, g, w_vals, dX, nout, st);
 }
 
 extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes) {
@@ -861,10 +825,13 @@ extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, 
     if (!bytes) return SP_ERR_INVALID_ARG;
     sp_status r = dims_of(s, nnz, d);
     if (r) return r;
-    const int64_t nt = wgrad_tiles(d);
-    *bytes = (nnz > 0 && d.B > 0)
-                 ? sp::align256((size_t)(nt + spt::reduce_blocks(nt)) * (size_t)spt::padded_cap(nnz) * 4)
-                 : 0;
+    if (nnz == 0 || d.B == 0) {
+        *bytes = 0;
+        return SP_OK;
+    }
+    const ConvPlan L = plan_layout(nullptr, d, nnz);
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, wgrad_tiles(d));
+    *bytes = sp::align256((size_t)sp2.nsplit * (size_t)spt2::part_stride(L.F) * 4);
     return SP_OK;
 }
 
@@ -883,24 +850,18 @@ extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const s
     if (d.B == 0) return zero_launch(dW, nnz, st);
     ConvPlan L = plan_layout(plan, d, nnz);
     const int64_t ntiles = wgrad_tiles(d);
-    // Slab splits: enough workgroups for four per compute unit where the
-    // (panel, token tile) grid alone is smaller.
-    const int nks = (int)std::max<int64_t>(
-        1, std::min<int64_t>(L.A.K, sp::ceil_div(4 * NUM_CU, std::max<int64_t>(L.A.P * ntiles, 1))));
-    const int64_t nwg = L.A.P * ntiles * nks;
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, ntiles);
+    const int64_t nwg = L.F.P * L.F.K * sp2.nsplit;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     ConvGeo<0> g = make_geo<0>(d, true);
     g.G = X;
     g.D = dY;
     float *part = (float *)workspace;
-    if (L.A.R == 128)
-        hipLaunchKernelGGL((spt::k_sddmm<8, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
-                           (int)ntiles, nks, L.A.cap, part);
-    else
-        hipLaunchKernelGGL((spt::k_sddmm<4, ConvGeo<0>>), dim3((unsigned)nwg), dim3(NTHR), 0, st, g, L.A.view(),
-                           (int)ntiles, nks, L.A.cap, part);
+    const int64_t pstride = spt2::part_stride(L.F);
+    hipLaunchKernelGGL((spt2::k_sddmm2<ConvGeo<0>, true>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, g, L.F.view(),
+                       (int)ntiles, sp2.nsplit, sp2.tps, part, pstride);
     SP_CHECK_LAUNCH();
-    return spt::sddmm_reduce(part, ntiles, L.A.cap, L.A.e_src, dW, part + ntiles * L.A.cap, st);
+    return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
 }
 
 extern "C" sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW, const int32_t *w_oc,

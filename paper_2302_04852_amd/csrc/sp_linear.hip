@@ -251,7 +251,8 @@ struct LinGeo2 {
     }
     // Accumulators -> Out through LDS: ys[position][token], then each thread
     // writes one row position for a stride of tokens (row segments coalesce).
-    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &, int64_t t0, int64_t row0) const {
+    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &, int64_t t0, int64_t row0,
+                          bool add) const {
         const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
         __syncthreads();
 #pragma unroll
@@ -268,7 +269,12 @@ struct LinGeo2 {
 #pragma unroll 4
             for (int t = tid / spt2::R; t < spt2::T; t += TSTEP) {
                 const int64_t gt = t0 + t;
-                if (gt < ntok) Out[gt * ldo + row] = ys[rl * spt2::YS + t];
+                if (gt < ntok) {
+                    if (add)
+                        unsafeAtomicAdd(Out + gt * ldo + row, ys[rl * spt2::YS + t]);
+                    else
+                        Out[gt * ldo + row] = ys[rl * spt2::YS + t];
+                }
             }
         }
     }
@@ -315,7 +321,7 @@ sp_status spmm_launch_t(const spt2::SlotTiling &t, const LinGeo2<MODE> &geo, con
     const int64_t nwg = t.P * ntiles;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     hipLaunchKernelGGL((spt2::k_spmm2<LinGeo2<MODE>>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals,
-                       t.view(), (int)ntiles);
+                       t.view(), (int)ntiles, 1);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
@@ -485,7 +491,7 @@ extern "C" sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64
     const int64_t pstride = spt2::part_stride(L.F);
     auto launch = [&](auto geo) {
         using G = decltype(geo);
-        hipLaunchKernelGGL((spt2::k_sddmm2<G>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, L.F.view(),
+        hipLaunchKernelGGL((spt2::k_sddmm2<G, false>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, L.F.view(),
                            (int)ntiles, sp2.nsplit, sp2.tps, part, pstride);
     };
     const int mode = (lin_mode(B, in_f) == 2 && out_f % 4 == 0) ? 2 : std::min(lin_mode(B, in_f), 1);

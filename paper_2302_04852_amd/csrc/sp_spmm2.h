@@ -167,14 +167,20 @@ struct MetaPipe {
 //   uint32_t load_chunk(pf, tok, c0)      unconditional loads of one chunk into registers,
 //                                         returns a validity mask
 //   write_chunk(xs, pf, mask, tok)        registers -> xs[column][64 tokens] (zero where invalid)
-//   store(ys, acc, tok, t0, row0)         accumulators -> output (through LDS)
+//   store(ys, acc, tok, t0, row0, add)   accumulators -> output (through LDS); with add,
+//                                         atomic adds into a zero-filled output
+// A workgroup takes one (panel, token tile) and a range of the chunks: small
+// problems split the chunks over nks = 2 workgroups, whose two partial
+// outputs meet in the zero-filled output by atomic adds -- exact and
+// independent of their order, since 0 + a + b = 0 + b + a.
 template <class Geo>
-__global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles) {
+__global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles,
+                                                int nks) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles);
-    const int p = L % tv.P, q = L / tv.P;
+    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks);
+    const int p = L % tv.P, q = (L / tv.P) % ntiles, ks = L / (tv.P * ntiles);
     const int64_t t0 = (int64_t)q * T;
     const int lp = 4 * (lane & 15) + (lane >> 4);  // this lane's entry within a metadata block
     const char *xb = reinterpret_cast<const char *>(xs) + (lane & 15) * 16;
@@ -188,14 +194,15 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
     for (int s = 0; s < NS; ++s) acc[s][0] = acc[s][1] = acc[s][2] = acc[s][3] = 0.f;
 
     const int K = tv.K;
+    const int k0 = (int)((int64_t)ks * K / nks), k1 = (int)((int64_t)(ks + 1) * K / nks);
     // Chunk k+1 is loaded after chunk k has been used: its registers are not
     // held through the product loop, and the second workgroup resident on
     // the compute unit covers the load latency.
-    for (int k = 0; k < K; ++k) {
+    for (int k = k0; k < k1; ++k) {
         {
             float pf[PF];
             const uint32_t pfm = geo.load_chunk(pf, tok, (int64_t)k * KC);
-            if (k > 0) __syncthreads();
+            if (k > k0) __syncthreads();
             geo.write_chunk(xs, pf, pfm, tok);
         }
         __syncthreads();
@@ -218,7 +225,7 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
             }
         }
     }
-    geo.store(xs, acc, tok, t0, (int64_t)p * R);
+    geo.store(xs, acc, tok, t0, (int64_t)p * R, nks > 1);
 }
 
 
@@ -301,7 +308,10 @@ __device__ inline int64_t slot_block(int bs, int nb, int jb) { return (int64_t)(
 
 // Geometry addition for the SDDMM:
 //   float4 load_dq(tok, t0, row0, s)   D[t0 + lane][rows of slot s of groups 0..3 of this wave]
-template <class Geo>
+// SKIP: skip the slots past the last one with blocks in a round -- for
+// narrow layers, which fill only the first slots of every wave (it costs the
+// full-panel case a few percent, so full panels are compiled without it).
+template <class Geo, bool SKIP>
 __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_sddmm2(Geo geo, SlotView tv, int ntiles, int nsplit, int tps,
                                                  float *__restrict__ part, int64_t pstride) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
@@ -343,6 +353,13 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
     for (int i = 0; i < NW; ++i) rounds = max(rounds, rounds_s[i]);
 
     for (int rho = 0; rho < rounds; ++rho) {
+        int nact = NS;
+        if (SKIP) {
+            nact = 0;
+#pragma unroll
+            for (int s = 0; s < NS; ++s)
+                if (nb[s] > rho * JMAX) nact = s + 1;
+        }
         float acc[NS][JMAX];
 #pragma unroll
         for (int s = 0; s < NS; ++s)
@@ -376,11 +393,12 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
                 // keep each slot's loads where they are: hoisting all slots'
                 // prefetches to the top of the unrolled loop costs registers
                 __builtin_amdgcn_sched_barrier(0);
+                if (SKIP && s >= nact) continue;
                 const float4 dq = dqn;
                 int off[JMAX];
 #pragma unroll
                 for (int jj = 0; jj < JMAX; ++jj) off[jj] = offn[jj];
-                if (s + 1 < NS) {
+                if (s + 1 < (SKIP ? nact : NS)) {
                     dqn = geo.load_dq(tok, t0, row0, s + 1);
 #pragma unroll
                     for (int jj = 0; jj < JMAX; ++jj)
