@@ -248,6 +248,11 @@ struct ConvGeo {
         const int tap = cb - ch * KK;
         int x = tap / KW;
         int y = tap - x * KW;
+        if (cb >= ncols) {  // the wave's columns are all past the last: nothing to load
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) pf[i] = 0.f;
+            return 0xffffffffu;
+        }
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             const bool col_ok = cb + i < ncols;
@@ -599,12 +604,14 @@ sp_status spmm_full(const spt2::SlotTiling &t, const Geo &geo, const float *vals
 // straight from global memory, neighbouring threads reading neighbouring
 // pixels.  A 256-row tile would leave all but one wave without rows here.
 constexpr int FR_MAX = 8;
-constexpr int FR_ENT = 2048;  // entries staged per round (32 KB)
+constexpr int FR_ENT = 2048;  // entries staged per round (at most 32 KB)
 
+// Dynamic LDS: min(entries, FR_ENT) * 16 bytes, so that small stems leave
+// room for more workgroups per compute unit.
 __global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__restrict__ ptr,
                                                  const int32_t *__restrict__ col, const int32_t *__restrict__ src,
                                                  const float *__restrict__ vals, int nrows) {
-    __shared__ int4 ent[FR_ENT];
+    extern __shared__ int4 ent[];
     const int tid = threadIdx.x;
     const int t = (int)blockIdx.x * 256 + tid;
     int a = TOK_INVALID, c = TOK_INVALID, gbase = 0, obase = -1;
@@ -667,10 +674,11 @@ __global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__
 }
 
 sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, const int32_t *src, const float *vals,
-                  int nrows, hipStream_t st) {
+                  int nrows, int64_t nent, hipStream_t st) {
     if (g.ntok == 0) return SP_OK;
-    hipLaunchKernelGGL(k_fewrows, dim3((unsigned)sp::ceil_div(g.ntok, 256)), dim3(256), 0, st, g, ptr, col, src, vals,
-                       nrows);
+    const size_t lds = (size_t)std::max<int64_t>(1, std::min<int64_t>(nent, FR_ENT)) * sizeof(int4);
+    hipLaunchKernelGGL(k_fewrows, dim3((unsigned)sp::ceil_div(g.ntok, 256)), dim3(256), lds, st, g, ptr, col, src,
+                       vals, nrows);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
@@ -678,10 +686,12 @@ sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, c
 // Input gradient of one unit-stride problem (the whole layer at stride 1, or
 // one phase of a stride-2 layer) over a CSR by input channel and its tiling.
 // nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
+// nnz bounds the entries of the part (the direct kernel's LDS size).
 sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,
-                         const int32_t *col, const int32_t *src, const float *vals, int nks, hipStream_t st) {
+                         const int32_t *col, const int32_t *src, const float *vals, int64_t nnz, int nks,
+                         hipStream_t st) {
     if (g.ntok == 0) return SP_OK;
-    if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, st);
+    if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, nnz, st);
     return spmm(t, g, vals, nks, st);
 }
 
@@ -793,7 +803,7 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         g.Out = dX;
         const int nks = d.IC <= FR_MAX ? 1 : spmm_splits(L.G, g.ntok);
         if (nks > 1 && (r = zero_launch(dX, nout, st))) return r;
-        return bwd_input_part(d, g, L.G, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nks, st);
+        return bwd_input_part(d, g, L.G, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nnz, nks, st);
     }
     if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
         ConvGeo<1> g[4];
@@ -810,7 +820,7 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         if (split && (r = zero_launch(dX, nout, st))) return r;
         for (int ph = 0; ph < 4; ++ph) {
             const ClassPart &cp = L.cls[(((ph >> 1) + d.ph) & 1) * 2 + (((ph & 1) + d.pw) & 1)];
-            if ((r = bwd_input_part(d, g[ph], cp.T, cp.ptr, cp.col, cp.src, w_vals, nks[ph], st))) return r;
+            if ((r = bwd_input_part(d, g[ph], cp.T, cp.ptr, cp.col, cp.src, w_vals, nnz, nks[ph], st))) return r;
         }
         return SP_OK;
     }
@@ -831,7 +841,7 @@ extern "C" sp_status sp_conv_bwd_weight_ws(const sp_conv_shape *s, int64_t nnz, 
     }
     const ConvPlan L = plan_layout(nullptr, d, nnz);
     const spt2::Split sp2 = spt2::sddmm_split(L.F, wgrad_tiles(d));
-    *bytes = sp::align256((size_t)sp2.nsplit * (size_t)spt2::part_stride(L.F) * 4);
+    *bytes = sp::align256((size_t)spt2::sddmm_ws_floats(L.F, sp2.nsplit) * 4);
     return SP_OK;
 }
 

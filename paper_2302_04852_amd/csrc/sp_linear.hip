@@ -461,7 +461,7 @@ extern "C" sp_status sp_linear_bwd_weight_ws(int64_t B, int64_t in_f, int64_t ou
     }
     const PlanLayout L = plan_layout(nullptr, in_f, out_f, nnz);
     const spt2::Split sp2 = spt2::sddmm_split(L.F, sp::ceil_div(B, spt2::T));
-    *bytes = sp::align256((size_t)sp2.nsplit * (size_t)spt2::part_stride(L.F) * 4);
+    *bytes = sp::align256((size_t)spt2::sddmm_ws_floats(L.F, sp2.nsplit) * 4);
     return SP_OK;
 }
 

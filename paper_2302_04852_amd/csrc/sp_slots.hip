@@ -110,13 +110,36 @@ __global__ __launch_bounds__(256) void k_slot_reduce(const int2 *__restrict__ me
     grad[e] = acc;
 }
 
+// First pass of the two-pass reduction: part2[g][pos] = the sum of splits
+// [RBLK*g, RBLK*g + RBLK) in order, one thread per (position, block).
+__global__ __launch_bounds__(256) void k_slot_reduce_blocks(const int2 *__restrict__ meta, int64_t npos,
+                                                            const float *__restrict__ part, int nsplit,
+                                                            int64_t pstride, float *__restrict__ part2) {
+    const int64_t pos = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int g = blockIdx.y;
+    if (pos >= npos || meta[pos].y < 0) return;
+    const int j1 = min(nsplit, (g + 1) * spt2::RBLK);
+    float acc = 0.f;
+    for (int j = g * spt2::RBLK; j < j1; ++j) acc += part[(int64_t)j * pstride + pos];
+    part2[(int64_t)g * pstride + pos] = acc;
+}
+
 }  // namespace
 
 namespace spt2 {
 
-sp_status slot_reduce(const SlotTiling &t, const float *part, int nsplit, int64_t pstride, float *grad,
+sp_status slot_reduce(const SlotTiling &t, float *part, int nsplit, int64_t pstride, float *grad,
                       hipStream_t st) {
     const int64_t npos = (t.nblk_cap + 1) * BLK;
+    if (nsplit > RBLK) {
+        const int nb2 = (int)sp::ceil_div(nsplit, RBLK);
+        float *part2 = part + (int64_t)nsplit * pstride;
+        hipLaunchKernelGGL(k_slot_reduce_blocks, dim3((unsigned)sp::ceil_div(npos, 256), (unsigned)nb2), dim3(256), 0,
+                           st, t.meta, npos, part, nsplit, pstride, part2);
+        SP_CHECK_LAUNCH();
+        part = part2;
+        nsplit = nb2;
+    }
     hipLaunchKernelGGL(k_slot_reduce, dim3((unsigned)sp::ceil_div(npos, 256)), dim3(256), 0, st, t.meta, npos, part,
                        nsplit, pstride, grad);
     SP_CHECK_LAUNCH();

@@ -469,9 +469,19 @@ inline Split sddmm_split(const SlotTiling &t, int64_t ntiles) {
 }
 // Floats per split in the SDDMM partial buffer.
 inline int64_t part_stride(const SlotTiling &t) { return (t.nblk_cap + 1) * BLK; }
+// Splits summed per thread in the first pass of a two-pass split reduction.
+constexpr int RBLK = 32;
+// Workspace floats of an SDDMM with nsplit splits: the partials, and the
+// block sums of the two-pass reduction when there are more than RBLK splits.
+inline int64_t sddmm_ws_floats(const SlotTiling &t, int nsplit) {
+    const int64_t nb2 = nsplit > RBLK ? sp::ceil_div(nsplit, RBLK) : 0;
+    return ((int64_t)nsplit + nb2) * part_stride(t);
+}
 
 // grad[e] = sum over the splits of part[split][pos] for the position pos of
 // entry e in the metadata blocks (fixed order; padding positions skipped).
-sp_status slot_reduce(const SlotTiling &t, const float *part, int nsplit, int64_t pstride, float *grad, hipStream_t st);
+// More than RBLK splits are summed in two passes: blocks of RBLK splits in
+// parallel into the workspace after the partials, then the block sums.
+sp_status slot_reduce(const SlotTiling &t, float *part, int nsplit, int64_t pstride, float *grad, hipStream_t st);
 
 }  // namespace spt2
