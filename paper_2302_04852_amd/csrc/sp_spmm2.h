@@ -365,6 +365,14 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
         for (int s = 0; s < NS; ++s)
 #pragma unroll
             for (int jj = 0; jj < JMAX; ++jj) acc[s][jj] = 0.f;
+        // The column offsets of the round's blocks depend on the (panel,
+        // chunk, wave, slot) only: loaded once per round, not per tile.
+        int off[NS][JMAX];
+#pragma unroll
+        for (int s = 0; s < NS; ++s)
+#pragma unroll
+            for (int jj = 0; jj < JMAX; ++jj)
+                off[s][jj] = (SKIP && s >= nact) ? 0 : tv.meta[slot_block(bs[s], nb[s], rho * JMAX + jj) + lp].x;
         for (int q = q0; q < q1; ++q) {
             const int64_t t0 = (int64_t)q * T;
             typename Geo::Tok tok;
@@ -380,14 +388,9 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
             // of the slot (one per group), the next slot's load in flight; a
             // per-wave LDS transpose hands lane (g, i) tokens 4i..4i+3 of row g.
             // LDS operations of one wave execute in order, so the read sees
-            // the writes and the next slot's writes follow this read.  The
-            // column offsets of the slot's blocks are likewise loaded one slot
-            // ahead (blocks past the slot's count read padding metadata).
+            // the writes and the next slot's writes follow this read.
             float *sc = dsx + w * (NG * T);
             float4 dqn = geo.load_dq(tok, t0, row0, 0);
-            int offn[JMAX];
-#pragma unroll
-            for (int jj = 0; jj < JMAX; ++jj) offn[jj] = tv.meta[slot_block(bs[0], nb[0], rho * JMAX + jj) + lp].x;
 #pragma unroll
             for (int s = 0; s < NS; ++s) {
                 // keep each slot's loads where they are: hoisting all slots'
@@ -395,15 +398,7 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
                 __builtin_amdgcn_sched_barrier(0);
                 if (SKIP && s >= nact) continue;
                 const float4 dq = dqn;
-                int off[JMAX];
-#pragma unroll
-                for (int jj = 0; jj < JMAX; ++jj) off[jj] = offn[jj];
-                if (s + 1 < (SKIP ? nact : NS)) {
-                    dqn = geo.load_dq(tok, t0, row0, s + 1);
-#pragma unroll
-                    for (int jj = 0; jj < JMAX; ++jj)
-                        offn[jj] = tv.meta[slot_block(bs[s + 1], nb[s + 1], rho * JMAX + jj) + lp].x;
-                }
+                if (s + 1 < (SKIP ? nact : NS)) dqn = geo.load_dq(tok, t0, row0, s + 1);
                 sc[0 * T + lane] = dq.x;
                 sc[1 * T + lane] = dq.y;
                 sc[2 * T + lane] = dq.z;
@@ -426,8 +421,8 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
 #pragma unroll
                             for (int i2 = 0; i2 < 8; i2 += 2) {
                                 float4 x0, x1, y0, y1;
-                                ld2(x0, x1, i2, off[jj], xb);
-                                ld2(y0, y1, i2 + 8, off[jj], xb);
+                                ld2(x0, x1, i2, off[s][jj], xb);
+                                ld2(y0, y1, i2 + 8, off[s][jj], xb);
                                 av[i2] = bfly8(dot4(d, x0), dot4(d, y0), gl);
                                 av[i2 + 1] = bfly8(dot4(d, x1), dot4(d, y1), gl);
                             }
@@ -435,7 +430,7 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
 #pragma unroll
                             for (int i2 = 0; i2 < 8; i2 += 2) {
                                 float4 x0, x1;
-                                ld2(x0, x1, i2, off[jj], xb);
+                                ld2(x0, x1, i2, off[s][jj], xb);
                                 av[i2] = bfly8(dot4(d, x0), 0.f, gl);
                                 av[i2 + 1] = bfly8(dot4(d, x1), 0.f, gl);
                             }
