@@ -24,9 +24,8 @@
 // Lane (g, i) of a wave loads entry (i, g) of a block -- one coalesced
 // 512-byte load per block -- and gathers its value; iteration i of group g
 // then broadcasts lane i of the group's 16-lane row to the whole group with
-// DPP row_newbcast.  Blocks of a wave's chunk are consecutive, so the next
-// blocks' metadata (two blocks ahead) and values (one block ahead) are
-// always in flight.
+// DPP row_newbcast.  The metadata and values are requested a slot or two
+// ahead of their use (see k_spmm2).
 #pragma once
 
 #include "sp_common.h"
@@ -131,34 +130,44 @@ __device__ inline void block16(float (&a)[4], int m, int off, float val, const c
     if (m > 12) { ld4<12>(x, off, xb); fma4x4<12>(a, val, x); }
 }
 
-// Metadata pipeline of one wave.  While block b is computed from (off, val),
-// the values of block b+1 are being gathered (m1 -> v1) and the metadata of
-// block b+2 is in flight (m2); neither request waits on the other.
-struct MetaPipe {
-    int off;
-    float val;
-    int2 m1, m2;
-    float v1;
-    int next;  // index of the block whose metadata is requested next
-    __device__ static float gather(const float *vals, int src) { return vals[src >= 0 ? src : 0]; }
-    __device__ void start(const SlotView &tv, const float *vals, int b0, int lp) {
-        const int2 m0 = tv.meta[(int64_t)b0 * BLK + lp];
-        m1 = tv.meta[(int64_t)(b0 + 1) * BLK + lp];
-        m2 = tv.meta[(int64_t)(b0 + 2) * BLK + lp];
-        off = m0.x;
-        val = m0.y >= 0 ? gather(vals, m0.y) : 0.f;
-        v1 = gather(vals, m1.y);
-        next = b0 + 3;
-    }
-    __device__ void advance(const SlotView &tv, const float *vals, int lp) {
-        off = m1.x;
-        val = m1.y >= 0 ? v1 : 0.f;
-        m1 = m2;
-        v1 = gather(vals, m1.y);
-        m2 = tv.meta[(int64_t)next * BLK + lp];
-        ++next;
+// Slot headers of one (panel, chunk, wave): the iteration count m of every
+// slot (packed as 16-bit halves) and the first block of every slot.
+struct SlotHdr {
+    int ms[NS], bs[NS];
+    // The header is read-only and its address wave-uniform: read through the
+    // constant address space it becomes scalar loads, which do not join the
+    // vector-memory queue that the metadata prefetches are waited on in.
+    __device__ void load(const SlotView &tv, int64_t p, int k, int w) {
+        typedef const __attribute__((address_space(4))) int32_t *cptr;
+        const cptr h = (cptr)(tv.hdr + ((p * tv.K + k) * NW + w) * HDR);
+        int run = h[0];
+#pragma unroll
+        for (int i = 0; i < NS / 2; ++i) {
+            const uint32_t v = (uint32_t)h[1 + i];
+            ms[2 * i] = (int)(v & 0xffffu);
+            ms[2 * i + 1] = (int)(v >> 16);
+        }
+#pragma unroll
+        for (int i = 0; i < NS; ++i) {
+            bs[i] = run;
+            run += (ms[i] + 15) / 16;
+        }
     }
 };
+
+// Metadata of the first PRE blocks of a slot, one entry per lane.  A slot
+// with fewer blocks requests its last block again (an unused, cached read) so
+// that no request goes to a block the slot does not own.
+constexpr int PRE = 2;
+__device__ inline void slot_meta(int2 (&m)[PRE], const SlotView &tv, int bs, int ms, int lp) {
+    const int nb = (ms + 15) / 16;
+#pragma unroll
+    for (int u = 0; u < PRE; ++u) m[u] = tv.meta[(int64_t)(bs + max(min(u, nb - 1), 0)) * BLK + lp];
+}
+__device__ inline void slot_vals(float (&v)[PRE], const int2 (&m)[PRE], const float *vals) {
+#pragma unroll
+    for (int u = 0; u < PRE; ++u) v[u] = vals[m[u].y >= 0 ? m[u].y : 0];
+}
 
 // --------------------------------------------------------------------------
 // Geometry interface (Geo), see sp_linear.hip / sp_conv.hip:
@@ -195,9 +204,25 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
 
     const int K = tv.K;
     const int k0 = (int)((int64_t)ks * K / nks), k1 = (int)((int64_t)(ks + 1) * K / nks);
-    // Chunk k+1 is loaded after chunk k has been used: its registers are not
-    // held through the product loop, and the second workgroup resident on
-    // the compute unit covers the load latency.
+    // Entry metadata is pipelined by slot, in registers indexed statically
+    // (the slots are unrolled), so no register holding a load in flight is
+    // ever copied: the metadata of slot s+2 is requested and the values of
+    // slot s+1 gathered when slot s starts, and the requests for the next
+    // chunk's first slots are issued during the current chunk's last ones.
+    // Every wait is then for a request made one or two slots earlier.  A slot
+    // with more than PRE blocks loads the rest on demand.
+    // Chunk k+1's operand is loaded after chunk k has been used: its registers
+    // are not held through the product loop, and the second workgroup
+    // resident on the compute unit covers the load latency.
+    SlotHdr hc, hn;
+    int2 mt[NS + 2][PRE];
+    float vv[NS + 1][PRE];
+    if (k0 < k1) {
+        hc.load(tv, p, k0, w);
+        slot_meta(mt[0], tv, hc.bs[0], hc.ms[0], lp);
+        slot_meta(mt[1], tv, hc.bs[1], hc.ms[1], lp);
+        slot_vals(vv[0], mt[0], vals);
+    }
     for (int k = k0; k < k1; ++k) {
         {
             float pf[PF];
@@ -206,22 +231,37 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
             geo.write_chunk(xs, pf, pfm, tok);
         }
         __syncthreads();
-        const int32_t *h = tv.hdr + (((int64_t)p * K + k) * NW + w) * HDR;
-        const int b0 = h[0];
-        int ms[NS];
-#pragma unroll
-        for (int i = 0; i < NS / 2; ++i) {
-            const uint32_t v = (uint32_t)h[1 + i];
-            ms[2 * i] = (int)(v & 0xffffu);
-            ms[2 * i + 1] = (int)(v >> 16);
-        }
-        MetaPipe mp;
-        mp.start(tv, vals, b0, lp);
+        const bool more = k + 1 < k1;
+        if (more) hn.load(tv, p, k + 1, w);
 #pragma unroll
         for (int s = 0; s < NS; ++s) {
-            for (int m = ms[s]; m > 0; m -= 16) {
-                block16(acc[s], m, mp.off, mp.val, xb);
-                mp.advance(tv, vals, lp);
+            if (s + 2 < NS)
+                slot_meta(mt[s + 2], tv, hc.bs[s + 2], hc.ms[s + 2], lp);
+            else if (more)
+                slot_meta(mt[s + 2], tv, hn.bs[s + 2 - NS], hn.ms[s + 2 - NS], lp);
+            if (s + 1 < NS || more) slot_vals(vv[s + 1], mt[s + 1], vals);
+            for (int blk = 0, m = hc.ms[s]; m > 0; ++blk, m -= 16) {
+                int off;
+                float val;
+                if (blk < PRE) {
+                    const int2 mb = blk == 0 ? mt[s][0] : mt[s][PRE - 1];
+                    off = mb.x;
+                    val = mb.y >= 0 ? (blk == 0 ? vv[s][0] : vv[s][PRE - 1]) : 0.f;
+                } else {
+                    const int2 mb = tv.meta[(int64_t)(hc.bs[s] + blk) * BLK + lp];
+                    off = mb.x;
+                    val = mb.y >= 0 ? vals[mb.y] : 0.f;
+                }
+                block16(acc[s], m, off, val, xb);
+            }
+        }
+        if (more) {
+            hc = hn;
+#pragma unroll
+            for (int u = 0; u < PRE; ++u) {
+                mt[0][u] = mt[NS][u];
+                mt[1][u] = mt[NS + 1][u];
+                vv[0][u] = vv[NS][u];
             }
         }
     }
