@@ -490,17 +490,32 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
     }
 }
 
-// Token splits of the SDDMM grid: enough workgroups to give every compute
-// unit two of them, each split a contiguous range of tps >= 1 token tiles.
+// Token splits of the SDDMM grid: each workgroup takes one (panel, chunk)
+// and a contiguous range of tps >= 1 token tiles.  The range length is chosen
+// to minimise the makespan ceil(workgroups / resident) * (tps + WG_COST),
+// where resident = 2 workgroups per compute unit (their LDS use) and WG_COST
+// (in tiles) stands for a workgroup's fixed work -- prologue, partial write,
+// its share of the split reduction.  A grid slightly larger than one
+// resident round would otherwise run a nearly empty second round.
+constexpr int64_t SDDMM_RESIDENT = 2 * 256;
 struct Split {
     int nsplit, tps;
 };
 inline Split sddmm_split(const SlotTiling &t, int64_t ntiles) {
     const int64_t pk = std::max<int64_t>(t.P * t.K, 1);
-    int64_t ns = std::max<int64_t>(1, std::min<int64_t>(sp::ceil_div(512, pk), ntiles));
-    const int64_t tps = std::max<int64_t>(1, sp::ceil_div(ntiles, ns));
-    ns = std::max<int64_t>(1, sp::ceil_div(ntiles, tps));
-    return Split{(int)ns, (int)tps};
+    ntiles = std::max<int64_t>(ntiles, 1);
+    int64_t best_tps = ntiles, best_cost = -1;
+    for (int64_t tps = ntiles; tps >= 1; --tps) {
+        const int64_t ns = sp::ceil_div(ntiles, tps);
+        constexpr int64_t WG_COST = 2;
+        const int64_t cost = sp::ceil_div(pk * ns, SDDMM_RESIDENT) * (tps + WG_COST);
+        if (best_cost < 0 || cost < best_cost) {
+            best_cost = cost;
+            best_tps = tps;
+        }
+        if (ns * pk > 64 * SDDMM_RESIDENT) break;  // far past any useful grid
+    }
+    return Split{(int)sp::ceil_div(ntiles, best_tps), (int)best_tps};
 }
 // Floats per split in the SDDMM partial buffer.
 inline int64_t part_stride(const SlotTiling &t) { return (t.nblk_cap + 1) * BLK; }
