@@ -205,6 +205,7 @@ struct ConvGeo {
     int sh, sw, ph, pw;
     float *Out;       // SpMM output [images][orows][onpix]
     const float *D;   // SDDMM stationary operand, same layout as Out
+    int obytes;       // size of Out / D in bytes (< 2 GiB)
     int orows;
     // Output pixel of the token at grid position (r, s): (r*osh + oa)*oW + s*osw + ob
     // (the identity map for the full pixel grid; a strided sub-grid for a phase).
@@ -214,30 +215,50 @@ struct ConvGeo {
     static_assert(CPW == spt2::PF, "one token and CPW columns per thread");
 
     struct Tok {
-        int a, c;   // spatial origin of the token (see tile_init)
-        int gbase;  // element offset of that origin in G
-        int obase;  // element offset of the token's output pixel in channel 0, -1 past the end
+        int a, c;      // spatial origin of the token (see tile_init)
+        uint32_t gbase4;  // byte offset of that origin in G (modulo 2^32)
+        int obase;     // element offset of the token's output pixel in channel 0, -1 past the end
+        uint32_t bad;  // DIR 0/1 with KK <= 32: bit x*KW + y set where tap (x, y) falls outside G
+        uint32_t dbase4;  // byte offset of obase in D, 2^31 (past any buffer range) past the end
     };
 
     __device__ void tile_init(Tok &tk, int64_t t0) const {
         const int t = (int)t0 + (int)(threadIdx.x & 63);
         tk.a = TOK_INVALID;
         tk.c = TOK_INVALID;
-        tk.gbase = 0;
+        tk.gbase4 = 0;
         tk.obase = -1;
+        tk.dbase4 = 0x80000000u;
         if (t < ntok) {
             const int b = t / npix, pix = t - b * npix;
             const int r = pix / tw, q = pix - r * tw;
             if (DIR == 0) {
                 tk.a = r * sh - ph;
                 tk.c = q * sw - pw;
-                tk.gbase = b * gimg + tk.a * gW + tk.c;
+                tk.gbase4 = (uint32_t)(b * gimg + tk.a * gW + tk.c) * 4u;
             } else {
                 tk.a = r + ph;
                 tk.c = q + pw;
-                tk.gbase = DIR == 1 ? b * gimg + tk.a * gW + tk.c : b * gimg;
+                tk.gbase4 = (uint32_t)(DIR == 1 ? b * gimg + tk.a * gW + tk.c : b * gimg) * 4u;
             }
             tk.obase = b * orows * onpix + (r * osh + oa) * oW + q * osw + ob;
+            tk.dbase4 = (uint32_t)tk.obase * 4u;
+        }
+        // Valid taps form a rectangle x in [x0, x1), y in [y0, y1) (empty past the end).
+        tk.bad = 0xffffffffu;
+        if (DIR != 2 && KK <= 32 && t < ntok) {
+            int x0, x1, y0, y1;
+            if (DIR == 0) {  // 0 <= a + x < gH
+                x0 = max(0, -tk.a), x1 = min(KH, gH - tk.a);
+                y0 = max(0, -tk.c), y1 = min(KW, gW - tk.c);
+            } else {  // 0 <= a - x < gH
+                x0 = max(0, tk.a - gH + 1), x1 = min(KH, tk.a + 1);
+                y0 = max(0, tk.c - gW + 1), y1 = min(KW, tk.c + 1);
+            }
+            if (y0 < y1) {
+                const uint32_t ym = ((y1 - y0 == 32) ? 0xffffffffu : ((1u << (y1 - y0)) - 1u)) << y0;
+                for (int x = x0; x < x1; ++x) tk.bad &= ~(ym << (x * KW));
+            }
         }
     }
 
@@ -253,6 +274,28 @@ struct ConvGeo {
             for (int i = 0; i < CPW; ++i) pf[i] = 0.f;
             return 0xffffffffu;
         }
+        if (DIR != 2 && KK <= 32 && cb + CPW <= ncols) {
+            // Offset = token part + wave-uniform column part; a tap outside G
+            // sets bit 31, which puts the offset past the buffer range (every
+            // valid offset is below 2^31), so the load returns 0.
+            int t = tap;
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) {
+                const int cofs = DIR == 0 ? ch * gplane + x * gW + y : ch * gplane - x * gW - y;
+                const uint32_t off = (tk.gbase4 + (uint32_t)cofs * 4u) | ((tk.bad >> t) << 31);
+                pf[i] = sp_raw_buffer_load_f32(rsrc, (int)off, 0, 0);
+                ++t;
+                if (++y == KW) {
+                    y = 0;
+                    if (++x == KH) {
+                        x = 0;
+                        t = 0;
+                        ++ch;
+                    }
+                }
+            }
+            return 0xffffffffu;
+        }
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             const bool col_ok = cb + i < ncols;
@@ -260,18 +303,18 @@ struct ConvGeo {
             int off;
             if (DIR == 0) {
                 ok = (unsigned)(tk.a + x) < (unsigned)gH && (unsigned)(tk.c + y) < (unsigned)gW;
-                off = tk.gbase + ch * gplane + x * gW + y;
+                off = ch * gplane + x * gW + y;
             } else if (DIR == 1) {
                 ok = (unsigned)(tk.a - x) < (unsigned)gH && (unsigned)(tk.c - y) < (unsigned)gW;
-                off = tk.gbase + ch * gplane - x * gW - y;
+                off = ch * gplane - x * gW - y;
             } else {
                 const int dh = tk.a - x, dw = tk.c - y;
                 const unsigned qh = (unsigned)dh / (unsigned)sh, qw = (unsigned)dw / (unsigned)sw;
                 ok = dh >= 0 && dw >= 0 && (int)qh * sh == dh && (int)qw * sw == dw && qh < (unsigned)gH &&
                      qw < (unsigned)gW;
-                off = tk.gbase + ch * gplane + (int)qh * gW + (int)qw;
+                off = ch * gplane + (int)qh * gW + (int)qw;
             }
-            pf[i] = sp_raw_buffer_load_f32(rsrc, (ok && col_ok) ? (int)((unsigned)off * 4u) : OOB, 0, 0);
+            pf[i] = sp_raw_buffer_load_f32(rsrc, (ok && col_ok) ? (int)(tk.gbase4 + (uint32_t)off * 4u) : OOB, 0, 0);
             if (++y == KW) {
                 y = 0;
                 if (++x == KH) {
@@ -318,15 +361,14 @@ struct ConvGeo {
     // D[token t0 + lane][rows of slot s of groups 0..3 of this wave], zero past
     // the last token or row.
     __device__ float4 load_dq(const Tok &tk, int64_t, int64_t row0, int s) const {
-        const int w = threadIdx.x >> 6;
-        const int64_t r = row0 + spt2::NG * spt2::NW * s + spt2::NG * w;
+        const sp_i32x4 rsrc = sp::make_rsrc(D, (uint32_t)obytes);
+        const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+        const int r = (int)row0 + spt2::NG * spt2::NW * s + spt2::NG * w;
         float v[4];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-            const bool ok = tk.obase >= 0 && r + g < orows;
-            const float u = D[ok ? tk.obase + (r + g) * onpix : 0];
-            v[g] = ok ? u : 0.f;
-        }
+        for (int g = 0; g < 4; ++g)
+            v[g] = r + g < orows ? sp_raw_buffer_load_f32(rsrc, (int)(tk.dbase4 + (uint32_t)((r + g) * onpix) * 4u), 0, 0)
+                                 : 0.f;
         return make_float4(v[0], v[1], v[2], v[3]);
     }
 };
@@ -520,6 +562,7 @@ ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
         g.gplane = (int)(d.H * d.W);
         g.gimg = (int)(d.IC * d.H * d.W);
         g.gbytes = (int)(d.B * d.IC * d.H * d.W * 4);
+        g.obytes = (int)(d.B * d.OC * d.OH * d.OW * 4);
         g.orows = (int)d.OC;
     } else {  // tokens = input pixels, G = dY, rows = IC
         g.ntok = (int)(d.B * d.H * d.W);
@@ -531,6 +574,7 @@ ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
         g.gplane = (int)(d.OH * d.OW);
         g.gimg = (int)(d.OC * d.OH * d.OW);
         g.gbytes = (int)(d.B * d.OC * d.OH * d.OW * 4);
+        g.obytes = (int)(d.B * d.IC * d.H * d.W * 4);
         g.orows = (int)d.IC;
     }
     g.onpix = g.npix;
