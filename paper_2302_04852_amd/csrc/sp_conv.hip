@@ -218,7 +218,7 @@ struct ConvGeo {
         int a, c;      // spatial origin of the token (see tile_init)
         uint32_t gbase4;  // byte offset of that origin in G (modulo 2^32)
         int obase;     // element offset of the token's output pixel in channel 0, -1 past the end
-        uint32_t bad;  // DIR 0/1 with KK <= 32: bit x*KW + y set where tap (x, y) falls outside G
+        uint32_t bad, bad_hi;  // DIR 0/1, KK <= 64: bit x*KW + y of (bad_hi:bad) set where tap (x, y) is outside G
         uint32_t dbase4;  // byte offset of obase in D, 2^31 (past any buffer range) past the end
     };
 
@@ -245,8 +245,8 @@ struct ConvGeo {
             tk.dbase4 = (uint32_t)tk.obase * 4u;
         }
         // Valid taps form a rectangle x in [x0, x1), y in [y0, y1) (empty past the end).
-        tk.bad = 0xffffffffu;
-        if (DIR != 2 && KK <= 32 && t < ntok) {
+        uint64_t bad = ~0ull;
+        if (DIR != 2 && KK <= 64 && t < ntok) {
             int x0, x1, y0, y1;
             if (DIR == 0) {  // 0 <= a + x < gH
                 x0 = max(0, -tk.a), x1 = min(KH, gH - tk.a);
@@ -256,8 +256,35 @@ struct ConvGeo {
                 y0 = max(0, tk.c - gW + 1), y1 = min(KW, tk.c + 1);
             }
             if (y0 < y1) {
-                const uint32_t ym = ((y1 - y0 == 32) ? 0xffffffffu : ((1u << (y1 - y0)) - 1u)) << y0;
-                for (int x = x0; x < x1; ++x) tk.bad &= ~(ym << (x * KW));
+                const uint64_t ym = ((y1 - y0 == 64) ? ~0ull : ((1ull << (y1 - y0)) - 1ull)) << y0;
+                for (int x = x0; x < x1; ++x) bad &= ~(ym << (x * KW));
+            }
+        }
+        tk.bad = (uint32_t)bad;
+        tk.bad_hi = (uint32_t)(bad >> 32);
+    }
+
+    // All CPW columns of the wave valid, KK <= 64.  Offset = token part +
+    // wave-uniform column part; a tap outside G sets bit 31, which puts the
+    // offset past the buffer range (every valid offset is below 2^31), so the
+    // load returns 0.  3 VALU per element (4 with 33..64 taps).
+    template <bool WIDE>
+    __device__ void load_masked(float (&pf)[spt2::PF], const Tok &tk, const sp_i32x4 &rsrc, int ch, int x, int y,
+                                int t) const {
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) {
+            const int cofs = DIR == 0 ? ch * gplane + x * gW + y : ch * gplane - x * gW - y;
+            const uint32_t word = WIDE && t >= 32 ? tk.bad_hi : tk.bad;
+            const uint32_t off = (tk.gbase4 + (uint32_t)cofs * 4u) | ((word >> (t & 31)) << 31);
+            pf[i] = sp_raw_buffer_load_f32(rsrc, (int)off, 0, 0);
+            ++t;
+            if (++y == KW) {
+                y = 0;
+                if (++x == KH) {
+                    x = 0;
+                    t = 0;
+                    ++ch;
+                }
             }
         }
     }
@@ -274,26 +301,11 @@ struct ConvGeo {
             for (int i = 0; i < CPW; ++i) pf[i] = 0.f;
             return 0xffffffffu;
         }
-        if (DIR != 2 && KK <= 32 && cb + CPW <= ncols) {
-            // Offset = token part + wave-uniform column part; a tap outside G
-            // sets bit 31, which puts the offset past the buffer range (every
-            // valid offset is below 2^31), so the load returns 0.
-            int t = tap;
-#pragma unroll
-            for (int i = 0; i < CPW; ++i) {
-                const int cofs = DIR == 0 ? ch * gplane + x * gW + y : ch * gplane - x * gW - y;
-                const uint32_t off = (tk.gbase4 + (uint32_t)cofs * 4u) | ((tk.bad >> t) << 31);
-                pf[i] = sp_raw_buffer_load_f32(rsrc, (int)off, 0, 0);
-                ++t;
-                if (++y == KW) {
-                    y = 0;
-                    if (++x == KH) {
-                        x = 0;
-                        t = 0;
-                        ++ch;
-                    }
-                }
-            }
+        if (DIR != 2 && KK <= 64 && cb + CPW <= ncols) {
+            if (KK <= 32)
+                load_masked<false>(pf, tk, rsrc, ch, x, y, tap);
+            else
+                load_masked<true>(pf, tk, rsrc, ch, x, y, tap);
             return 0xffffffffu;
         }
 #pragma unroll
@@ -731,6 +743,27 @@ sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, c
 // one phase of a stride-2 layer) over a CSR by input channel and its tiling.
 // nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
 // nnz bounds the entries of the part (the direct kernel's LDS size).
+// The four phases of a stride-2 input gradient as one launch: the phases of
+// small layers have a few dozen token tiles each, far too few for the chip
+// when launched one after another.  Block b runs work item b - begin[ph] of
+// the phase whose range [begin[ph], begin[ph+1]) holds b.  Blocks are not
+// regrouped by XCD: consecutive blocks go to different XCDs, so each XCD gets
+// its share of every phase (phases with no taps only write zeros).
+struct PhaseSet {
+    ConvGeo<1> g[4];
+    spt2::SlotView tv[4];
+    int ntiles[4], nks[4];
+    int begin[5];
+};
+
+__global__ __launch_bounds__(spt2::NTHR) void k_spmm2_phases(PhaseSet ps, const float *__restrict__ vals) {
+    const int L = blockIdx.x;
+    int ph = 0;
+#pragma unroll
+    for (int i = 1; i < 4; ++i) ph += L >= ps.begin[i];
+    spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph]);
+}
+
 sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,
                          const int32_t *col, const int32_t *src, const float *vals, int64_t nnz, int nks,
                          hipStream_t st) {
@@ -860,6 +893,36 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
             g[ph].Out = dX;
             nks[ph] = d.IC <= FR_MAX ? 1 : spmm_splits(cp.T, g[ph].ntok);
             split |= nks[ph] > 1;
+        }
+        if (d.IC > FR_MAX) {
+            // One launch over the four phases; the chunk split is decided on
+            // the total number of work items.
+            PhaseSet ps;
+            int64_t items = 0;
+            for (int ph = 0; ph < 4; ++ph) {
+                const ClassPart &cp = L.cls[(((ph >> 1) + d.ph) & 1) * 2 + (((ph & 1) + d.pw) & 1)];
+                ps.g[ph] = g[ph];
+                ps.tv[ph] = cp.T.view();
+                ps.ntiles[ph] = (int)sp::ceil_div(g[ph].ntok, spt2::T);
+                items += cp.T.P * ps.ntiles[ph];
+            }
+            split = 0;
+            for (int ph = 0; ph < 4; ++ph) {
+                ps.nks[ph] = (items < NUM_CU && ps.tv[ph].K >= 2) ? 2 : 1;
+                split |= ps.nks[ph] > 1;
+            }
+            int64_t total = 0;
+            for (int ph = 0; ph < 4; ++ph) {
+                ps.begin[ph] = (int)total;
+                total += (int64_t)ps.tv[ph].P * ps.ntiles[ph] * ps.nks[ph];
+                if (total > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+            }
+            ps.begin[4] = (int)total;
+            if (split && (r = zero_launch(dX, nout, st))) return r;
+            if (total == 0) return SP_OK;
+            hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)total), dim3(spt2::NTHR), 0, st, ps, w_vals);
+            SP_CHECK_LAUNCH();
+            return SP_OK;
         }
         if (split && (r = zero_launch(dX, nout, st))) return r;
         for (int ph = 0; ph < 4; ++ph) {

@@ -178,17 +178,18 @@ __device__ inline void slot_vals(float (&v)[PRE], const int2 (&m)[PRE], const fl
 //   write_chunk(xs, pf, mask, tok)        registers -> xs[column][64 tokens] (zero where invalid)
 //   store(ys, acc, tok, t0, row0, add)   accumulators -> output (through LDS); with add,
 //                                         atomic adds into a zero-filled output
-// A workgroup takes one (panel, token tile) and a range of the chunks: small
-// problems split the chunks over nks = 2 workgroups, whose two partial
-// outputs meet in the zero-filled output by atomic adds -- exact and
-// independent of their order, since 0 + a + b = 0 + b + a.
+// Work item L in [0, P*ntiles*nks) is one (panel, token tile) and a range of
+// the chunks: small problems split the chunks over nks = 2 workgroups, whose
+// two partial outputs meet in the zero-filled output by atomic adds -- exact
+// and independent of their order, since 0 + a + b = 0 + b + a.  spmm2_tile
+// runs one work item in the calling workgroup; k_spmm2 launches the items of
+// one product, a kernel may also pick among several products by block.
 template <class Geo>
-__global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles,
-                                                int nks) {
+__device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const SlotView &tv, int ntiles, int nks,
+                           int L) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int L = sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks);
     const int p = L % tv.P, q = (L / tv.P) % ntiles, ks = L / (tv.P * ntiles);
     const int64_t t0 = (int64_t)q * T;
     const int lp = 4 * (lane & 15) + (lane >> 4);  // this lane's entry within a metadata block
@@ -266,6 +267,12 @@ __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict
         }
     }
     geo.store(xs, acc, tok, t0, (int64_t)p * R, nks > 1);
+}
+
+template <class Geo>
+__global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles,
+                                                int nks) {
+    spmm2_tile(geo, vals, tv, ntiles, nks, sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks));
 }
 
 

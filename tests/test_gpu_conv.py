@@ -210,6 +210,8 @@ SMALL = [
     (3, 20, 10, 7, 9, 2, 4, (2, 2), (1, 2), 0.5),        # stride 2, even kernel sizes
     (2, 1, 15, 15, 8, 5, 5, (2, 2), (2, 2), 0.4),        # one input channel (direct kernel), stride 2
     (2, 8, 6, 6, 300, 3, 3, (1, 1), (1, 1), 0.9),        # 8 input channels, 2700 columns (entry rounds)
+    (1, 300, 9, 8, 24, 3, 3, (2, 2), (1, 1), 0.8),       # stride 2 with two input-channel panels
+    (2, 16, 20, 20, 40, 7, 7, (1, 1), (3, 3), 0.9),      # 49 taps over full waves (wide tap masks)
 ]
 
 
