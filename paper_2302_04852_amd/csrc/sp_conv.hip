@@ -34,6 +34,8 @@ namespace {
 constexpr int OOB = 0x7ffffff0;       // byte offset beyond any accepted buffer range
 constexpr int TOK_INVALID = -(1 << 28);  // spatial origin of tokens past the end
 constexpr int64_t MAX_BYTES = 0x7fff0000LL;
+// The staging's multiply-high divisions n / d (d <= 32) are exact for n < 2^26.
+constexpr int TABLE_MAX_COLS = 1 << 25;
 
 // --------------------------------------------------------------------------
 // Encoders: dense pattern [OC][IC][KH][KW] -> five arrays.  One wave per
@@ -201,6 +203,7 @@ struct ConvGeo {
     int npix, tw;     // pixels per image of the token grid and its width
     int ncols;        // channels of G * KH * KW
     int KH, KW, KK;
+    uint32_t kk_m, kw_m;  // ceil(2^31 / KK), ceil(2^31 / KW): n / d = mulhi(2n, m) for 0 <= n < 2^15
     int gH, gW, gplane, gimg;  // G: plane height/width, plane size, image size (elements)
     int sh, sw, ph, pw;
     float *Out;       // SpMM output [images][orows][onpix]
@@ -218,7 +221,10 @@ struct ConvGeo {
         int a, c;      // spatial origin of the token (see tile_init)
         uint32_t gbase4;  // byte offset of that origin in G (modulo 2^32)
         int obase;     // element offset of the token's output pixel in channel 0, -1 past the end
-        uint32_t bad, bad_hi;  // DIR 0/1, KK <= 64: bit x*KW + y of (bad_hi:bad) set where tap (x, y) is outside G
+        // DIR 0/1, KK <= 32: (bad_hi:bad) has bit j set where tap j mod KK
+        // (tap x*KW + y) is outside G -- the tap mask repeated, so that bits
+        // t..t+31 describe 32 consecutive columns starting at tap t.
+        uint32_t bad, bad_hi;
         uint32_t dbase4;  // byte offset of obase in D, 2^31 (past any buffer range) past the end
     };
 
@@ -244,9 +250,11 @@ struct ConvGeo {
             tk.obase = b * orows * onpix + (r * osh + oa) * oW + q * osw + ob;
             tk.dbase4 = (uint32_t)tk.obase * 4u;
         }
-        // Valid taps form a rectangle x in [x0, x1), y in [y0, y1) (empty past the end).
+        // Valid taps form a rectangle x in [x0, x1), y in [y0, y1) (empty past
+        // the end).  KK >= 1 keeps the doubling loop finite (an empty tap
+        // class has no columns and never stages).
         uint64_t bad = ~0ull;
-        if (DIR != 2 && KK <= 64 && t < ntok) {
+        if (DIR != 2 && KK >= 1 && KK <= 32 && t < ntok) {
             int x0, x1, y0, y1;
             if (DIR == 0) {  // 0 <= a + x < gH
                 x0 = max(0, -tk.a), x1 = min(KH, gH - tk.a);
@@ -256,58 +264,57 @@ struct ConvGeo {
                 y0 = max(0, tk.c - gW + 1), y1 = min(KW, tk.c + 1);
             }
             if (y0 < y1) {
-                const uint64_t ym = ((y1 - y0 == 64) ? ~0ull : ((1ull << (y1 - y0)) - 1ull)) << y0;
+                const uint64_t ym = ((1ull << (y1 - y0)) - 1ull) << y0;
                 for (int x = x0; x < x1; ++x) bad &= ~(ym << (x * KW));
             }
+            bad &= (1ull << KK) - 1ull;
+            for (int len = KK; len < 64; len *= 2) bad |= bad << len;
         }
         tk.bad = (uint32_t)bad;
         tk.bad_hi = (uint32_t)(bad >> 32);
     }
 
-    // All CPW columns of the wave valid, KK <= 64.  Offset = token part +
-    // wave-uniform column part; a tap outside G sets bit 31, which puts the
-    // offset past the buffer range (every valid offset is below 2^31), so the
-    // load returns 0.  3 VALU per element (4 with 33..64 taps).
-    template <bool WIDE>
-    __device__ void load_masked(float (&pf)[spt2::PF], const Tok &tk, const sp_i32x4 &rsrc, int ch, int x, int y,
-                                int t) const {
+    // Byte offsets of the wave's CPW columns for this thread's token, past the
+    // buffer range where the element is outside G, past the last column or
+    // past the last token.  The loads are issued afterwards from one place.
+    //
+    // Table path (DIR 0/1, KK <= 32, all CPW columns valid): lane l of each
+    // 16-lane row computes the column offsets of columns cb + l and
+    // cb + 16 + l once; element i takes its offset from lane i & 15 by DPP,
+    // folded into the add, and bit 31 from bit i of the token's repeated tap
+    // mask shifted by the first column's tap, which lifts the offset past the
+    // buffer range (every valid offset is below 2^31).  3 VALU per element
+    // and no per-element scalar bookkeeping.
+    __device__ void offsets_table(uint32_t (&o)[spt2::PF], const Tok &tk, int cb, int t0) const {
+        const int l = threadIdx.x & 15;
+        int tab[2];
 #pragma unroll
-        for (int i = 0; i < CPW; ++i) {
-            const int cofs = DIR == 0 ? ch * gplane + x * gW + y : ch * gplane - x * gW - y;
-            const uint32_t word = WIDE && t >= 32 ? tk.bad_hi : tk.bad;
-            const uint32_t off = (tk.gbase4 + (uint32_t)cofs * 4u) | ((word >> (t & 31)) << 31);
-            pf[i] = sp_raw_buffer_load_f32(rsrc, (int)off, 0, 0);
-            ++t;
-            if (++y == KW) {
-                y = 0;
-                if (++x == KH) {
-                    x = 0;
-                    t = 0;
-                    ++ch;
-                }
-            }
+        for (int h = 0; h < 2; ++h) {
+            const uint32_t n = (uint32_t)(cb + 16 * h + l);
+            const uint32_t c = __umulhi(2u * n, kk_m);
+            const uint32_t t = n - c * (uint32_t)KK;
+            const uint32_t xx = __umulhi(2u * t, kw_m);
+            const uint32_t yy = t - xx * (uint32_t)KW;
+            const int cofs = DIR == 0 ? (int)(c * gplane + xx * gW + yy) : (int)(c * gplane) - (int)(xx * gW + yy);
+            tab[h] = cofs * 4;
+        }
+        const uint32_t B = (uint32_t)((((uint64_t)tk.bad_hi << 32) | tk.bad) >> t0);
+        offsets_table_at<0>(o, tk, tab, B);
+    }
+    template <int I>
+    __device__ void offsets_table_at(uint32_t (&o)[spt2::PF], const Tok &tk, const int (&tab)[2], uint32_t B) const {
+        if constexpr (I < CPW) {
+            const uint32_t off = tk.gbase4 + (uint32_t)spt2::bcast16<I & 15>(tab[I >> 4]);
+            o[I] = off | ((B << (31 - I)) & 0x80000000u);
+            offsets_table_at<I + 1>(o, tk, tab, B);
         }
     }
-
-    __device__ uint32_t load_chunk(float (&pf)[spt2::PF], const Tok &tk, int64_t c0) const {
-        const sp_i32x4 rsrc = sp::make_rsrc(G, (uint32_t)gbytes);
-        const int cb = (int)c0 + CPW * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    // General path: a scalar walk over (channel, x, y) with explicit tests.
+    __device__ void offsets_walk(uint32_t (&o)[spt2::PF], const Tok &tk, int cb) const {
         int ch = cb / KK;
         const int tap = cb - ch * KK;
         int x = tap / KW;
         int y = tap - x * KW;
-        if (cb >= ncols) {  // the wave's columns are all past the last: nothing to load
-#pragma unroll
-            for (int i = 0; i < CPW; ++i) pf[i] = 0.f;
-            return 0xffffffffu;
-        }
-        if (DIR != 2 && KK <= 64 && cb + CPW <= ncols) {
-            if (KK <= 32)
-                load_masked<false>(pf, tk, rsrc, ch, x, y, tap);
-            else
-                load_masked<true>(pf, tk, rsrc, ch, x, y, tap);
-            return 0xffffffffu;
-        }
 #pragma unroll
         for (int i = 0; i < CPW; ++i) {
             const bool col_ok = cb + i < ncols;
@@ -326,7 +333,7 @@ struct ConvGeo {
                      qw < (unsigned)gW;
                 off = ch * gplane + (int)qh * gW + (int)qw;
             }
-            pf[i] = sp_raw_buffer_load_f32(rsrc, (ok && col_ok) ? (int)(tk.gbase4 + (uint32_t)off * 4u) : OOB, 0, 0);
+            o[i] = (ok && col_ok) ? tk.gbase4 + (uint32_t)off * 4u : (uint32_t)OOB;
             if (++y == KW) {
                 y = 0;
                 if (++x == KH) {
@@ -335,6 +342,23 @@ struct ConvGeo {
                 }
             }
         }
+    }
+
+    __device__ uint32_t load_chunk(float (&pf)[spt2::PF], const Tok &tk, int64_t c0) const {
+        const int cb = (int)c0 + CPW * __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+        if (cb >= ncols) {  // the wave's columns are all past the last: nothing to load
+#pragma unroll
+            for (int i = 0; i < CPW; ++i) pf[i] = 0.f;
+            return 0xffffffffu;
+        }
+        uint32_t o[spt2::PF];
+        if (DIR != 2 && KK <= 32 && ncols <= TABLE_MAX_COLS && cb + CPW <= ncols)
+            offsets_table(o, tk, cb, cb % KK);
+        else
+            offsets_walk(o, tk, cb);
+        const sp_i32x4 rsrc = sp::make_rsrc(G, (uint32_t)gbytes);
+#pragma unroll
+        for (int i = 0; i < CPW; ++i) pf[i] = sp_raw_buffer_load_f32(rsrc, (int)o[i], 0, 0);
         return 0xffffffffu;
     }
 
@@ -554,6 +578,14 @@ sp_status classes_build(const ConvPlan &L, const Dims &d, const uint8_t *w_x, co
     return SP_OK;
 }
 
+// Multipliers of the staging's divisions by KK and KW (0 for an empty class).
+template <int DIR>
+void set_tap_magic(ConvGeo<DIR> &g) {
+    const uint64_t two31 = 1ull << 31;
+    g.kk_m = g.KK > 0 ? (uint32_t)((two31 + g.KK - 1) / g.KK) : 0;
+    g.kw_m = g.KW > 0 ? (uint32_t)((two31 + g.KW - 1) / g.KW) : 0;
+}
+
 template <int DIR>
 ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
     ConvGeo<DIR> g{};
@@ -589,6 +621,7 @@ ConvGeo<DIR> make_geo(const Dims &d, bool fwd_tokens) {
         g.obytes = (int)(d.B * d.IC * d.H * d.W * 4);
         g.orows = (int)d.IC;
     }
+    set_tap_magic(g);
     g.onpix = g.npix;
     g.oW = g.tw;
     g.osh = g.osw = 1;
@@ -611,6 +644,7 @@ ConvGeo<1> phase_geo(const Dims &d, int a, int b, const TapClass &tc) {
     g.KH = tc.ncx;
     g.KW = tc.ncy;
     g.KK = tc.ncx * tc.ncy;
+    set_tap_magic(g);
     g.ncols = (int)(d.OC * g.KK);
     g.ph = (a + d.ph - tc.cx) / 2;
     g.pw = (b + d.pw - tc.cy) / 2;
