@@ -97,13 +97,9 @@ __device__ inline void fma4(float (&a)[4], float v, const float4 &x) {
 
 // One block of up to 16 iterations, four at a time.  ld4<I> issues the LDS
 // reads of iterations I..I+3 (the column offset of iteration i is broadcast
-// from lane i of the group's 16-lane row by DPP row_newbcast, folded into
-// the address add); fma4x4<I> multiplies them with the value broadcast from
-// the same lanes, by DPP inside the FMA itself.  The reads of the next four
-// iterations are issued before the current four are multiplied; every exit
-// path has its own exact wait.  The compiler does not see DPP inside inline
-// assembly, so each group of sixteen FMAs starts with s_nop 1: the two wait
-// states a VALU write of a VGPR needs before a DPP read of it.
+// from lane i of the group's 16-lane row by DPP row_newbcast, which the
+// compiler folds into the address add); fma4x4<I> multiplies them with the
+// value broadcast from the same lanes (one DPP move per iteration, four FMAs).
 template <int I>
 __device__ inline void ld4(float4 (&x)[4], int off, const char *xb) {
     x[0] = *reinterpret_cast<const float4 *>(xb + bcast16<I + 0>(off));
