@@ -21,6 +21,12 @@ before the timed region; the mask structure (plan) is prepared once outside
 it, as the method prescribes (masks change rarely), and its preparation time
 is reported separately.
 
+Timing: W untimed steps; then K steps with an event pair around every op for
+the per-op times and the roofline (event records between ops add gaps of
+their own; that pass's step time is reported as `ms_per_step_with_op_events`);
+then K steps between two HIP events with nothing recorded in between: the
+step time and `value`.
+
 Prints ONE JSON line.  Extra fields: `roofline` (dominant kernel: algorithmic
 bytes / FLOPs per launch over its event-timed duration), `cpu_baseline` (the
 CPU oracle timed on the host over a bounded sample, about 10 s), `ops`
@@ -50,8 +56,8 @@ WORKLOADS = ("ffn", "linear_small", "conv3x3_56", "conv_sweep", "resnet18")
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", choices=WORKLOADS, default="ffn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -62,7 +68,7 @@ def parse():
 
 
 COPY_BYTES = 1 << 30
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm2_k_sddmm2_ffn_pair_hbm_traffic.txt")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm2_k_bwd_fused_ffn_pair_hbm_traffic.txt")
 KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", "sp_linear.hip"]
 
 
@@ -106,11 +112,15 @@ def calibrate_copy():
 # ------------------------------------------------------------ algorithmic cost
 
 def linear_alg_bytes(op, B, in_f, out_f, nnz):
-    """Minimum bytes an op must move: dense operands once, values+indices once."""
+    """Minimum bytes an op must move: dense operands once, values+indices once.
+    "bwd" is both gradients in one pass: dY, X and dX once, values, indices
+    and dW once."""
     if op == "fwd":
         return 4 * B * in_f + 4 * B * out_f + 8 * nnz + 4 * (out_f + 1)
     if op == "bwd_input":
         return 4 * B * out_f + 4 * B * in_f + 8 * nnz + 4 * (in_f + 1)
+    if op == "bwd":
+        return 4 * B * out_f + 8 * B * in_f + 12 * nnz + 4 * (in_f + 1) + 4 * (out_f + 1)
     return 4 * B * (in_f + out_f) + 8 * nnz + 4 * (out_f + 1)
 
 
@@ -208,9 +218,12 @@ class ConvLayer:
 # --------------------------------------------------------------------- timing
 
 def time_ops(torch, ops, steps, warmup):
-    """W untimed steps, then K steps between two events on the launch stream,
-    with an event pair around every op inside the timed region.  Returns the
-    step time (ms) and the mean time of every op (ms)."""
+    """W untimed steps; then K steps with an event pair around every op (the
+    per-op times; the event records between the ops add gaps of their own);
+    then K steps between two events on the launch stream with nothing
+    recorded in between (the step time).  Returns the step time (ms), the
+    mean time of every op (ms) and the step time of the instrumented pass
+    (ms)."""
     def step():
         for op in ops:
             op[1]()
@@ -236,7 +249,15 @@ def time_ops(torch, ops, steps, warmup):
     for k in range(steps):
         for i, (a, b) in enumerate(evs[k]):
             per_op[i] += a.elapsed_time(b)
-    return e0.elapsed_time(e1) / steps, [t / steps for t in per_op]
+    ms_instr = e0.elapsed_time(e1) / steps
+
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for _ in range(steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / steps, [t / steps for t in per_op], ms_instr
 
 
 def op_row(ms, fl, by):
@@ -305,46 +326,50 @@ def run_linear(args, sp, torch, which):
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
 
     def lin_op(name, L, kind, f):
-        return (name, f, kind, 2.0 * L.nnz * B, linear_alg_bytes(kind, B, L.in_f, L.out_f, L.nnz), L)
+        flops = (4.0 if kind == "bwd" else 2.0) * L.nnz * B
+        return (name, f, kind, flops, linear_alg_bytes(kind, B, L.in_f, L.out_f, L.nnz), L)
 
+    # The backward of a layer is one sp_linear_bwd call: the input gradient
+    # and the weight gradient in one launch (plus the fixed-order reduction).
     if which == "ffn":
         ops = [
             lin_op("W1.fwd", L1, "fwd",
                    lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
             lin_op("W2.fwd", L2, "fwd",
                    lambda: sp.sp_linear_fwd(Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, Y2)),
-            lin_op("W2.bwd_input", L2, "bwd_input",
-                   lambda: sp.sp_linear_bwd_input(dY2, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, dX2)),
-            lin_op("W2.bwd_weight", L2, "bwd_weight",
-                   lambda: sp.sp_linear_bwd_weight(dY2, Y1, B, L2.in_f, L2.out_f, L2.nnz, L2.plan, L2.dW, ws)),
-            lin_op("W1.bwd_input", L1, "bwd_input",
-                   lambda: sp.sp_linear_bwd_input(dX2, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1)),
-            lin_op("W1.bwd_weight", L1, "bwd_weight",
-                   lambda: sp.sp_linear_bwd_weight(dX2, X, B, L1.in_f, L1.out_f, L1.nnz, L1.plan, L1.dW, ws)),
+            lin_op("W2.bwd", L2, "bwd",
+                   lambda: sp.sp_linear_bwd(dY2, Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, dX2, L2.dW,
+                                            ws)),
+            lin_op("W1.bwd", L1, "bwd",
+                   lambda: sp.sp_linear_bwd(dX2, X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1, L1.dW,
+                                            ws)),
         ]
     else:
         ops = [
             lin_op("fwd", L1, "fwd",
                    lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
-            lin_op("bwd_input", L1, "bwd_input",
-                   lambda: sp.sp_linear_bwd_input(dY1, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1)),
-            lin_op("bwd_weight", L1, "bwd_weight",
-                   lambda: sp.sp_linear_bwd_weight(dY1, X, B, L1.in_f, L1.out_f, L1.nnz, L1.plan, L1.dW, ws)),
+            lin_op("bwd", L1, "bwd",
+                   lambda: sp.sp_linear_bwd(dY1, X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1, L1.dW,
+                                            ws)),
         ]
-    ms_per_step, per_op = time_ops(torch, ops, args.steps, args.warmup)
+    ms_per_step, per_op, ms_instr = time_ops(torch, ops, args.steps, args.warmup)
     flops_step = sum(o[3] for o in ops)
     bytes_step = sum(o[4] for o in ops)
 
-    # Dominant kernel: the SpMM kernel serves fwd and bwd_input (equal
-    # algorithmic work per launch); the SDDMM kernel serves bwd_weight.
-    spmm = [t for o, t in zip(ops, per_op) if o[2] in ("fwd", "bwd_input")]
-    sddmm = [t for o, t in zip(ops, per_op) if o[2] == "bwd_weight"]
-    if sum(sddmm) >= sum(spmm):
-        dom, dom_ms, kind = "k_sddmm2+k_slot_reduce", float(np.mean(sddmm)), "bwd_weight"
+    # Dominant kernel: the SpMM kernel serves the forward passes; the fused
+    # backward kernel (input-gradient SpMM and weight-gradient SDDMM in one
+    # launch, then the split reduction) the backward passes.  Both layers of
+    # the pair have the same nnz and the same work per launch.
+    spmm = [t for o, t in zip(ops, per_op) if o[2] == "fwd"]
+    bwd = [t for o, t in zip(ops, per_op) if o[2] == "bwd"]
+    if sum(bwd) >= sum(spmm):
+        dom, dom_ms, kind = "k_bwd_fused+k_slot_reduce", float(np.mean(bwd)), "bwd"
     else:
         dom, dom_ms, kind = "k_spmm2", float(np.mean(spmm)), "fwd"
-    fl = 2.0 * L1.nnz * B
-    by = linear_alg_bytes(kind, B, L1.in_f, L1.out_f, L1.nnz)
+    # per launch: the mean over the launches of that kind (the two layers'
+    # backward passes move different dense bytes)
+    fl = float(np.mean([o[3] for o in ops if o[2] == kind]))
+    by = float(np.mean([o[4] for o in ops if o[2] == kind]))
     traffic = measured_traffic(dom) if which == "ffn" else None
     if which == "ffn":
         config = {"workload": "FFN pair W1 768->3072 + W2 3072->768, 95% unstructured sparse, 8192 tokens, "
@@ -355,6 +380,7 @@ def run_linear(args, sp, torch, which):
                   "tokens": B, "sparsity": 0.90, "nnz": L1.nnz}
     out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
     out["hbm"] = hbm_record(bytes_step, ms_per_step)
+    out["ms_per_step_with_op_events"] = round(ms_instr, 5)
     out["roofline"] = roofline(dom, kind, fl, by, dom_ms, traffic, {"source_hash": kernel_source_hash()})
     out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
     out["plan_ms"] = {L.name: round(L.plan_ms, 3) for L in layers}
@@ -407,7 +433,7 @@ def run_conv(args, sp, torch, which):
                         ("bwd_weight", lambda: sp.sp_linear_bwd_weight(dY, X, B, i_f, o_f, fc.nnz, fc.plan, fc.dW,
                                                                        ws))):
             ops.append(("fc." + kind, f, kind, 2.0 * fc.nnz * B, linear_alg_bytes(kind, B, i_f, o_f, fc.nnz), fc))
-    ms_per_step, per_op = time_ops(torch, ops, args.steps, args.warmup)
+    ms_per_step, per_op, ms_instr = time_ops(torch, ops, args.steps, args.warmup)
     flops_step = sum(o[3] for o in ops)
     bytes_step = sum(o[4] for o in ops)
     # Dominant kernel: the conv op kind with the largest total time; its
@@ -426,6 +452,7 @@ def run_conv(args, sp, torch, which):
               "nnz_total": int(sum(L.nnz for L in layers) + (fc.nnz if fc else 0))}
     out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
     out["hbm"] = hbm_record(bytes_step, ms_per_step)
+    out["ms_per_step_with_op_events"] = round(ms_instr, 5)
     out["roofline"] = roofline(CONV_KERNEL[kind], kind, fl / n, by / n, t / n, None,
                                {"launches_per_step": n, "note": "per-launch means over the workload's layers"})
     out["by_op"] = {k: {"ms": round(v[0], 4), "tflops": round(v[1] / v[0] / 1e9, 3),

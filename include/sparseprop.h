@@ -166,6 +166,19 @@ sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64_t B,
                                const void *plan, float *dW, void *workspace,
                                size_t ws_bytes, void *stream);
 
+/* Backward pass of one layer, both gradients (Sec. 3.2, Eqs. 1-2; the
+ * paper's Algorithm 1 computes them together): the results of
+ * sp_linear_bwd_input (dX) and sp_linear_bwd_weight (dW), bit for bit, from
+ * one launch of both products plus the fixed-order reduction.  Arguments as
+ * in those two calls; the workspace is sp_linear_bwd_weight_ws() bytes.
+ * Shapes the fused kernel does not cover (in_f or out_f not a multiple of
+ * 64, operands of 2 GiB or more, B == 0, nnz == 0) run the two calls one
+ * after the other on the stream. */
+sp_status sp_linear_bwd(const float *dY, const float *X, int64_t B, int64_t in_f,
+                        int64_t out_f, const float *vals, int64_t nnz,
+                        const void *plan, float *dX, float *dW, void *workspace,
+                        size_t ws_bytes, void *stream);
+
 /* Host.  Structural check of a CSR pattern held in HOST memory: returns
  * SP_OK or SP_ERR_INVALID_ARG (row_ptr not monotone, row_ptr[0] != 0,
  * row_ptr[out_f] != nnz, column out of range or not strictly ascending). */

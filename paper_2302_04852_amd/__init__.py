@@ -63,6 +63,7 @@ _SIGS = {
     "sp_linear_bwd_input": [_P, _I64, _I64, _I64, _P, _I64, _P, _P, _P],
     "sp_linear_bwd_weight_ws": [_I64, _I64, _I64, _I64, ctypes.POINTER(_SZ)],
     "sp_linear_bwd_weight": [_P, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _SZ, _P],
+    "sp_linear_bwd": [_P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_linear_validate": [_I64, _I64, _P, _P, _I64],
     "sp_conv_out_hw": [ctypes.POINTER(ConvShape), ctypes.POINTER(_I64), ctypes.POINTER(_I64)],
     "sp_conv_encode_rows": [_I64, _I64, _I32, _I32, _P, _P, _P, _P],
@@ -184,6 +185,12 @@ def sp_linear_bwd_weight_ws(B, in_f, out_f, nnz):
 def sp_linear_bwd_weight(dY, X, B, in_f, out_f, nnz, plan, dW, workspace, stream=None):
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("sp_linear_bwd_weight", _ptr(dY), _ptr(X), B, in_f, out_f, nnz, _ptr(plan), _ptr(dW),
+          _ptr(workspace), nbytes, _stream(stream))
+
+
+def sp_linear_bwd(dY, X, B, in_f, out_f, vals, nnz, plan, dX, dW, workspace, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _call("sp_linear_bwd", _ptr(dY), _ptr(X), B, in_f, out_f, _ptr(vals), nnz, _ptr(plan), _ptr(dX), _ptr(dW),
           _ptr(workspace), nbytes, _stream(stream))
 
 

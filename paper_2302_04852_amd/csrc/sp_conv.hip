@@ -795,7 +795,8 @@ __global__ __launch_bounds__(spt2::NTHR) void k_spmm2_phases(PhaseSet ps, const 
     int ph = 0;
 #pragma unroll
     for (int i = 1; i < 4; ++i) ph += L >= ps.begin[i];
-    spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph]);
+    __shared__ __attribute__((aligned(16))) float xs[spt2::XS_FLOATS];
+    spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph], xs);
 }
 
 sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,

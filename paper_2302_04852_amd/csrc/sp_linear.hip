@@ -445,6 +445,35 @@ extern "C" sp_status sp_linear_fwd(const float *X, int64_t B, int64_t in_f, int6
     return spmm_launch(L.F, X, B, in_f, Y, out_f, vals, nnz, (hipStream_t)stream);
 }
 
+// The input gradient (SpMM over the CSC tiling) and the weight gradient
+// (SDDMM over the row tiling) of one layer in one launch.  The two products
+// are independent; workgroups of both kinds sharing the compute units hide
+// part of each other's staging and metadata latency, and the tail of one
+// product fills with work of the other.  Each XCD gets a contiguous share of
+// the SDDMM items (long-running: a token range each) followed by a
+// contiguous share of the SpMM items, so both keep the L2 locality of the
+// single products and the SpMM items fill the slots the SDDMM leaves.  Both
+// kinds stage through one LDS chunk buffer.
+template <class GA, class GB>
+__global__ __launch_bounds__(spt2::NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_bwd_fused(
+    GA ga, const float *__restrict__ vals, spt2::SlotView tvA, int ntilesA, int nA, GB gb, spt2::SlotView tvB,
+    int ntilesB, int tps, float *__restrict__ part, int64_t pstride, int nB) {
+    __shared__ __attribute__((aligned(16))) float xs[spt2::XS_FLOATS];
+    __shared__ spt2::SddmmLds sl;
+    const int total = nA + nB;
+    // XCD x runs blocks x, x+8, ...: cnt of them, the first cntp blocks of the
+    // XCD order (all XCDs before x) precede them.  Its share of the SDDMM
+    // items comes first, then its share of the SpMM items.
+    const int b = blockIdx.x, x = b % 8, kx = b / 8;
+    const int per = total / 8, rem = total % 8;
+    const int cntp = x * per + min(x, rem), cnt = per + (x < rem);
+    const int b0 = (int)((int64_t)cntp * nB / total), b1 = (int)((int64_t)(cntp + cnt) * nB / total);
+    if (kx < b1 - b0)
+        spt2::sddmm2_tile<GB, false>(gb, tvB, ntilesB, tps, part, pstride, b0 + kx, xs, sl);
+    else
+        spt2::spmm2_tile(ga, vals, tvA, ntilesA, 1, (cntp - b0) + (kx - (b1 - b0)), xs);
+}
+
 extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f, const float *vals,
                                          int64_t nnz, const void *plan, float *dX, void *stream) {
     if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
@@ -501,6 +530,37 @@ extern "C" sp_status sp_linear_bwd_weight(const float *dY, const float *X, int64
         launch(LinGeo2<1>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
     else
         launch(LinGeo2<0>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f});
+    SP_CHECK_LAUNCH();
+    return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
+}
+
+extern "C" sp_status sp_linear_bwd(const float *dY, const float *X, int64_t B, int64_t in_f, int64_t out_f,
+                                   const float *vals, int64_t nnz, const void *plan, float *dX, float *dW,
+                                   void *workspace, size_t ws_bytes, void *stream) {
+    if (B < 0 || bad_dims(in_f, out_f, nnz) || !plan) return SP_ERR_INVALID_ARG;
+    if ((B * in_f > 0 && !dX) || (B * out_f > 0 && !dY) || (nnz > 0 && (!vals || !dW))) return SP_ERR_INVALID_ARG;
+    if (B > 0 && nnz > 0 && !X) return SP_ERR_INVALID_ARG;
+    size_t need;
+    sp_linear_bwd_weight_ws(B, in_f, out_f, nnz, &need);
+    if (nnz > 0 && B > 0 && (!workspace || ws_bytes < need)) return SP_ERR_WORKSPACE;
+    const bool fused = B > 0 && nnz > 0 && lin_mode(B, out_f) == 2 && lin_mode(B, in_f) == 2 && out_f % 4 == 0;
+    if (!fused) {  // the two passes one after the other on the stream
+        sp_status r = sp_linear_bwd_input(dY, B, in_f, out_f, vals, nnz, plan, dX, stream);
+        if (r) return r;
+        return sp_linear_bwd_weight(dY, X, B, in_f, out_f, nnz, plan, dW, workspace, ws_bytes, stream);
+    }
+    hipStream_t st = (hipStream_t)stream;
+    PlanLayout L = plan_layout(plan, in_f, out_f, nnz);
+    const int64_t ntiles = sp::ceil_div(B, spt2::T);
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, ntiles);
+    const int64_t nA = L.G.P * ntiles, nB = L.F.P * L.F.K * sp2.nsplit;
+    if (nA + nB > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    float *part = (float *)workspace;
+    const int64_t pstride = spt2::part_stride(L.F);
+    hipLaunchKernelGGL((k_bwd_fused<LinGeo2<2>, LinGeo2<2>>), dim3((unsigned)(nA + nB)), dim3(spt2::NTHR), 0, st,
+                       LinGeo2<2>{dY, B, out_f, out_f, dX, in_f, in_f, nullptr, 0}, vals, L.G.view(), (int)ntiles,
+                       (int)nA, LinGeo2<2>{X, B, in_f, in_f, nullptr, 0, out_f, dY, out_f}, L.F.view(), (int)ntiles,
+                       sp2.tps, part, pstride, (int)nB);
     SP_CHECK_LAUNCH();
     return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
 }

@@ -178,12 +178,12 @@ __device__ inline void slot_vals(float (&v)[PRE], const int2 (&m)[PRE], const fl
 // the chunks: small problems split the chunks over nks = 2 workgroups, whose
 // two partial outputs meet in the zero-filled output by atomic adds -- exact
 // and independent of their order, since 0 + a + b = 0 + b + a.  spmm2_tile
-// runs one work item in the calling workgroup; k_spmm2 launches the items of
-// one product, a kernel may also pick among several products by block.
+// runs one work item in the calling workgroup, staging through xs (LDS,
+// XS_FLOATS floats); k_spmm2 launches the items of one product, a kernel may
+// also pick among several products by block.
 template <class Geo>
 __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const SlotView &tv, int ntiles, int nks,
-                           int L) {
-    __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
+                           int L, float *xs) {
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int p = L % tv.P, q = (L / tv.P) % ntiles, ks = L / (tv.P * ntiles);
@@ -268,7 +268,8 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
 template <class Geo>
 __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles,
                                                 int nks) {
-    spmm2_tile(geo, vals, tv, ntiles, nks, sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks));
+    __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
+    spmm2_tile(geo, vals, tv, ntiles, nks, sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks), xs);
 }
 
 
@@ -354,16 +355,21 @@ __device__ inline int64_t slot_block(int bs, int nb, int jb) { return (int64_t)(
 // SKIP: skip the slots past the last one with blocks in a round -- for
 // narrow layers, which fill only the first slots of every wave (it costs the
 // full-panel case a few percent, so full panels are compiled without it).
+// LDS of one SDDMM workgroup beyond the staged chunk.
+struct SddmmLds {
+    float dsx[NW * NG * T];  // per-wave D transpose scratch
+    int rounds[NW];
+};
+
+// Work item L in [0, P*K*nsplit): one (panel, chunk) and token range L / (P*K).
 template <class Geo, bool SKIP>
-__global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_sddmm2(Geo geo, SlotView tv, int ntiles, int nsplit, int tps,
-                                                 float *__restrict__ part, int64_t pstride) {
-    __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
-    __shared__ __attribute__((aligned(16))) float dsx[NW * NG * T];  // per-wave D transpose scratch
-    __shared__ int rounds_s[NW];
+__device__ void sddmm2_tile(const Geo &geo, const SlotView &tv, int ntiles, int tps, float *__restrict__ part,
+                            int64_t pstride, int L, float *xs, SddmmLds &sl) {
+    float *dsx = sl.dsx;
+    int *rounds_s = sl.rounds;
     const int tid = threadIdx.x, lane = tid & 63;
     const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int P = tv.P, K = tv.K;
-    const int L = sp::xcd_remap(blockIdx.x, P * K * nsplit);
     const int p = L % P, k = (L / P) % K, j = L / (P * K);
     const int q0 = j * tps, q1 = min(ntiles, q0 + tps);
     const int lp = 4 * (lane & 15) + (lane >> 4);
@@ -491,6 +497,15 @@ __global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) vo
                 if (jb < nb[s]) part[(int64_t)j * pstride + (int64_t)(bs[s] + jb) * BLK + lp] = acc[s][jj];
             }
     }
+}
+
+template <class Geo, bool SKIP>
+__global__ __launch_bounds__(NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_sddmm2(
+    Geo geo, SlotView tv, int ntiles, int nsplit, int tps, float *__restrict__ part, int64_t pstride) {
+    __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
+    __shared__ SddmmLds sl;
+    sddmm2_tile<Geo, SKIP>(geo, tv, ntiles, tps, part, pstride, sp::xcd_remap(blockIdx.x, tv.P * tv.K * nsplit), xs,
+                           sl);
 }
 
 // Token splits of the SDDMM grid: each workgroup takes one (panel, chunk)

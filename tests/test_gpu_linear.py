@@ -92,6 +92,18 @@ class GpuLayer:
         return dW[:self.nnz]
 
 
+    def bwd(self, dY, X):
+        """Both gradients from sp_linear_bwd."""
+        import torch
+        B = X.shape[0]
+        ws = torch.empty(max(self.sp.sp_linear_bwd_weight_ws(B, self.in_f, self.out_f, self.nnz), 1),
+                         dtype=torch.uint8, device="cuda")
+        dX = torch.full((B, self.in_f), float("nan"), device="cuda")
+        dW = torch.full((max(self.nnz, 1),), float("nan"), device="cuda")
+        self.sp.sp_linear_bwd(dY, X, B, self.in_f, self.out_f, self.vals, self.nnz, self.plan, dX, dW, ws)
+        return dX, dW[:self.nnz]
+
+
 def _run_all(sp, orc, mask, W, X, dY, name):
     import torch
     _say("case %s: out=%d in=%d B=%d nnz=%d" % (name, mask.shape[0], mask.shape[1], X.shape[0], int(mask.sum())))
@@ -108,6 +120,11 @@ def _run_all(sp, orc, mask, W, X, dY, name):
     assert_parity(dX.cpu().numpy(), dXr, dXa, name + " bwd_input")
     dWr, dWa = orc.linear_bwd_weight(dY, X, L.o_rp, L.o_ci)
     assert_parity(dW.cpu().numpy(), dWr, dWa, name + " bwd_weight")
+    # both gradients in one call: the same kernels, so the same bits
+    dXf, dWf = L.bwd(dYd, Xd)
+    torch.cuda.synchronize()
+    assert torch.equal(dXf, dX), name + " sp_linear_bwd dX differs from sp_linear_bwd_input"
+    assert torch.equal(dWf, dW), name + " sp_linear_bwd dW differs from sp_linear_bwd_weight"
     return L, Y, dX, dW
 
 
@@ -145,6 +162,8 @@ def test_small_layer_seed0(sp, orc):
     (300, 150, 100, 1.0),     # dense: several staging rounds per tile
     (1, 1, 1, 1.0),
     (64, 33, 9, 0.5),         # in_f not a multiple of 4 (scalar staging path)
+    (320, 192, 300, 0.08),    # multiples of 64: the one-launch backward, ragged tokens
+    (64, 512, 65, 0.2),       # one row panel, one token past a tile
 ])
 def test_ragged_shapes(sp, orc, out_f, in_f, B, density):
     rng = np.random.default_rng(out_f * 7 + in_f * 3 + B)
