@@ -13,7 +13,8 @@ Other workloads (``--workload``), each timed the same way:
                 each at 80/90/95/98%;
   resnet18      the 20 convolutions and the FC layer of a ResNet-18 at batch 64,
                 224x224, 95% (sparse passes only; activations drawn per layer).
-A step is the forward, input gradient and weight gradient of every layer.
+A step is the forward, input gradient and weight gradient of every layer; the
+two gradients of a layer come from one sp_linear_bwd / sp_conv_bwd call.
 
 Metric: effective GFLOP/s = sum over ops of 2 * nnz * tokens (linear) or
 2 * nnz * B * OH * OW (conv), divided by the step time.  Inputs live in HBM
@@ -132,6 +133,13 @@ def conv_alg_bytes(B, IC, H, W, OC, OH, OW, nnz):
     return 4 * B * IC * H * W + 4 * B * OC * OH * OW + 6 * nnz + 2 * OC * (IC + 1) + 4 * (OC + 1)
 
 
+def conv_bwd_alg_bytes(B, IC, H, W, OC, OH, OW, nnz):
+    """Both gradients in one pass: X read and dX written, dY read once; per
+    stored entry its value read, its gradient written and its two taps; the
+    two index arrays."""
+    return 8 * B * IC * H * W + 4 * B * OC * OH * OW + 10 * nnz + 2 * OC * (IC + 1) + 4 * (OC + 1)
+
+
 def bound_of(flops, nbytes):
     """Roofline bound of an op: HBM when its arithmetic intensity is below the
     ridge point (peak FLOP/s over peak B/s), else the FP32 ALU."""
@@ -203,15 +211,15 @@ class ConvLayer:
         B, IC, H, W, OC, KH, KW = self.dims
         fl = 2.0 * self.nnz * B * self.OH * self.OW
         by = conv_alg_bytes(B, IC, H, W, OC, self.OH, self.OW, self.nnz)
+        by_b = conv_bwd_alg_bytes(B, IC, H, W, OC, self.OH, self.OW, self.nnz)
+        # the backward is one sp_conv_bwd call: input and weight gradient
         return [
             (self.name + ".fwd", lambda: sp.sp_conv_fwd(self.X, self.shape, self.w_vals, self.nnz, self.plan, self.Y),
              "fwd", fl, by, self),
-            (self.name + ".bwd_input",
-             lambda: sp.sp_conv_bwd_input(self.dY, self.shape, self.w_vals, self.nnz, self.plan, self.dX),
-             "bwd_input", fl, by, self),
-            (self.name + ".bwd_weight",
-             lambda: sp.sp_conv_bwd_weight(self.dY, self.X, self.shape, self.nnz, self.plan, self.dW, self.ws),
-             "bwd_weight", fl, by, self),
+            (self.name + ".bwd",
+             lambda: sp.sp_conv_bwd(self.dY, self.X, self.shape, self.w_vals, self.nnz, self.plan, self.dX, self.dW,
+                                    self.ws),
+             "bwd", 2 * fl, by_b, self),
         ]
 
 
@@ -406,8 +414,8 @@ CONV_DESC = {
     "resnet18": "ResNet-18 sparse layers at batch 64, 224x224, 95%: the 20 convolutions and the FC 512->1000; "
                 "fwd, bwd_input, bwd_weight of every layer (BN/ReLU/pooling not included)",
 }
-CONV_KERNEL = {"fwd": "k_spmm2<ConvGeo<0>>", "bwd_input": "k_spmm2<ConvGeo<1|2>> / k_fewrows",
-               "bwd_weight": "k_sddmm2<ConvGeo<0>>+k_slot_reduce"}
+CONV_KERNEL = {"fwd": "k_spmm2<ConvGeo<0>>",
+               "bwd": "k_conv_bwd_fused+k_slot_reduce (<= 8 input channels: k_fewrows, then the SDDMM)"}
 
 
 def run_conv(args, sp, torch, which):
@@ -429,10 +437,10 @@ def run_conv(args, sp, torch, which):
         dX = torch.empty(B, i_f, device="cuda")
         ws = torch.empty(max(sp.sp_linear_bwd_weight_ws(B, i_f, o_f, fc.nnz), 1), dtype=torch.uint8, device="cuda")
         for kind, f in (("fwd", lambda: sp.sp_linear_fwd(X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, Y)),
-                        ("bwd_input", lambda: sp.sp_linear_bwd_input(dY, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, dX)),
-                        ("bwd_weight", lambda: sp.sp_linear_bwd_weight(dY, X, B, i_f, o_f, fc.nnz, fc.plan, fc.dW,
-                                                                       ws))):
-            ops.append(("fc." + kind, f, kind, 2.0 * fc.nnz * B, linear_alg_bytes(kind, B, i_f, o_f, fc.nnz), fc))
+                        ("bwd", lambda: sp.sp_linear_bwd(dY, X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, dX, fc.dW,
+                                                         ws))):
+            ops.append(("fc." + kind, f, kind, (4.0 if kind == "bwd" else 2.0) * fc.nnz * B,
+                        linear_alg_bytes(kind, B, i_f, o_f, fc.nnz), fc))
     ms_per_step, per_op, ms_instr = time_ops(torch, ops, args.steps, args.warmup)
     flops_step = sum(o[3] for o in ops)
     bytes_step = sum(o[4] for o in ops)

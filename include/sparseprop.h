@@ -266,6 +266,17 @@ sp_status sp_conv_bwd_weight(const float *dY, const float *X, const sp_conv_shap
                              int64_t nnz, const void *plan, float *dW, void *workspace,
                              size_t ws_bytes, void *stream);
 
+/* Backward pass of one conv layer, both gradients (Sec. 3.3, Eqs. 4-5; the
+ * paper's Algorithm 2 computes them together): the results of
+ * sp_conv_bwd_input (dX) and sp_conv_bwd_weight (dW), bit for bit.  For more
+ * than 8 input channels and stride 1 or 2 (both directions) both products
+ * run in one launch, followed by the fixed-order reduction; other layers run
+ * the two calls one after the other on the stream.  Arguments as in those
+ * calls; the workspace is sp_conv_bwd_weight_ws() bytes. */
+sp_status sp_conv_bwd(const float *dY, const float *X, const sp_conv_shape *s,
+                      const float *w_vals, int64_t nnz, const void *plan, float *dX,
+                      float *dW, void *workspace, size_t ws_bytes, void *stream);
+
 /* Host.  Structural check of a five-array pattern held in HOST memory. */
 sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW,
                            const int32_t *w_oc, const int16_t *w_ic,

@@ -75,6 +75,7 @@ _SIGS = {
     "sp_conv_bwd_input": [_P, ctypes.POINTER(ConvShape), _P, _I64, _P, _P, _P],
     "sp_conv_bwd_weight_ws": [ctypes.POINTER(ConvShape), _I64, ctypes.POINTER(_SZ)],
     "sp_conv_bwd_weight": [_P, _P, ctypes.POINTER(ConvShape), _I64, _P, _P, _P, _SZ, _P],
+    "sp_conv_bwd": [_P, _P, ctypes.POINTER(ConvShape), _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_conv_validate": [_I64, _I64, _I32, _I32, _P, _P, _P, _P, _I64],
 }
 
@@ -247,6 +248,12 @@ def sp_conv_bwd_weight_ws(shape: ConvShape, nnz):
 def sp_conv_bwd_weight(dY, X, shape: ConvShape, nnz, plan, dW, workspace, stream=None):
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("sp_conv_bwd_weight", _ptr(dY), _ptr(X), ctypes.byref(shape), nnz, _ptr(plan), _ptr(dW),
+          _ptr(workspace), nbytes, _stream(stream))
+
+
+def sp_conv_bwd(dY, X, shape: ConvShape, w_vals, nnz, plan, dX, dW, workspace, stream=None):
+    nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _call("sp_conv_bwd", _ptr(dY), _ptr(X), ctypes.byref(shape), _ptr(w_vals), nnz, _ptr(plan), _ptr(dX), _ptr(dW),
           _ptr(workspace), nbytes, _stream(stream))
 
 

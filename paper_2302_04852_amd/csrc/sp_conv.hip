@@ -809,6 +809,70 @@ sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTil
 
 int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, spt2::T); }
 
+// Input-gradient work items of a layer with more than FR_MAX input channels
+// and stride 1 (one part: the input-channel-major tiling) or 2 (the four
+// phases over their tap classes).  Stride 1 splits its chunks as the
+// single-product launch does, stride 2 on the total items of its phases, so
+// either kind of launch computes the same sums.  split: dX must be zero-filled
+// first.
+sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, float *dX, PhaseSet &ps, bool &split) {
+    int64_t items = 0;
+    split = false;
+    if (d.sh == 1 && d.sw == 1) {
+        ConvGeo<1> g = make_geo<1>(d, false);
+        g.G = dY;
+        g.Out = dX;
+        for (int ph = 0; ph < 4; ++ph) {
+            ps.g[ph] = g;
+            ps.tv[ph] = L.G.view();
+            ps.ntiles[ph] = ph == 0 ? (int)sp::ceil_div(g.ntok, spt2::T) : 0;
+            ps.nks[ph] = ph == 0 ? spmm_splits(L.G, g.ntok) : 1;
+        }
+    } else {
+        for (int ph = 0; ph < 4; ++ph) {
+            const int a = ph >> 1, b = ph & 1;
+            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
+            ps.g[ph] = phase_geo(d, a, b, cp.tc);
+            ps.g[ph].G = dY;
+            ps.g[ph].Out = dX;
+            ps.tv[ph] = cp.T.view();
+            ps.ntiles[ph] = (int)sp::ceil_div(ps.g[ph].ntok, spt2::T);
+            items += cp.T.P * ps.ntiles[ph];
+        }
+        for (int ph = 0; ph < 4; ++ph) ps.nks[ph] = (items < NUM_CU && ps.tv[ph].K >= 2) ? 2 : 1;
+    }
+    int64_t total = 0;
+    for (int ph = 0; ph < 4; ++ph) {
+        ps.begin[ph] = (int)total;
+        total += (int64_t)ps.tv[ph].P * ps.ntiles[ph] * ps.nks[ph];
+        split |= ps.nks[ph] > 1 && ps.ntiles[ph] > 0;
+        if (total > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    }
+    ps.begin[4] = (int)total;
+    return SP_OK;
+}
+
+// Both gradients of a unit-stride or stride-2 layer in one launch: the
+// weight-gradient SDDMM items and the input-gradient SpMM items of the phase
+// set share the grid (each XCD runs its share of the SDDMM items first, then
+// of the SpMM items), so workgroups of both kinds on a compute unit hide part
+// of each other's staging and metadata latency.
+__global__ __launch_bounds__(spt2::NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_conv_bwd_fused(
+    PhaseSet ps, const float *__restrict__ vals, ConvGeo<0> gw, spt2::SlotView tvF, int ntilesW, int tps,
+    float *__restrict__ part, int64_t pstride, int nB) {
+    __shared__ __attribute__((aligned(16))) float xs[spt2::XS_FLOATS];
+    __shared__ spt2::SddmmLds sl;
+    int idx;
+    if (spt2::xcd_split2(blockIdx.x, ps.begin[4], nB, idx)) {
+        spt2::sddmm2_tile<ConvGeo<0>, true>(gw, tvF, ntilesW, tps, part, pstride, idx, xs, sl);
+    } else {
+        int ph = 0;
+#pragma unroll
+        for (int i = 1; i < 4; ++i) ph += idx >= ps.begin[i];
+        spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], idx - ps.begin[ph], xs);
+    }
+}
+
 }  // namespace
 
 // ==========================================================================
@@ -918,51 +982,25 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         return bwd_input_part(d, g, L.G, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nnz, nks, st);
     }
     if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
-        ConvGeo<1> g[4];
-        int nks[4], split = 0;
-        for (int ph = 0; ph < 4; ++ph) {
-            const int a = ph >> 1, b = ph & 1;
-            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
-            g[ph] = phase_geo(d, a, b, cp.tc);
-            g[ph].G = dY;
-            g[ph].Out = dX;
-            nks[ph] = d.IC <= FR_MAX ? 1 : spmm_splits(cp.T, g[ph].ntok);
-            split |= nks[ph] > 1;
-        }
         if (d.IC > FR_MAX) {
             // One launch over the four phases; the chunk split is decided on
             // the total number of work items.
             PhaseSet ps;
-            int64_t items = 0;
-            for (int ph = 0; ph < 4; ++ph) {
-                const ClassPart &cp = L.cls[(((ph >> 1) + d.ph) & 1) * 2 + (((ph & 1) + d.pw) & 1)];
-                ps.g[ph] = g[ph];
-                ps.tv[ph] = cp.T.view();
-                ps.ntiles[ph] = (int)sp::ceil_div(g[ph].ntok, spt2::T);
-                items += cp.T.P * ps.ntiles[ph];
-            }
-            split = 0;
-            for (int ph = 0; ph < 4; ++ph) {
-                ps.nks[ph] = (items < NUM_CU && ps.tv[ph].K >= 2) ? 2 : 1;
-                split |= ps.nks[ph] > 1;
-            }
-            int64_t total = 0;
-            for (int ph = 0; ph < 4; ++ph) {
-                ps.begin[ph] = (int)total;
-                total += (int64_t)ps.tv[ph].P * ps.ntiles[ph] * ps.nks[ph];
-                if (total > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
-            }
-            ps.begin[4] = (int)total;
+            bool split;
+            if ((r = input_grad_set(d, L, dY, dX, ps, split))) return r;
             if (split && (r = zero_launch(dX, nout, st))) return r;
-            if (total == 0) return SP_OK;
-            hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)total), dim3(spt2::NTHR), 0, st, ps, w_vals);
+            if (ps.begin[4] == 0) return SP_OK;
+            hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
             SP_CHECK_LAUNCH();
             return SP_OK;
         }
-        if (split && (r = zero_launch(dX, nout, st))) return r;
-        for (int ph = 0; ph < 4; ++ph) {
-            const ClassPart &cp = L.cls[(((ph >> 1) + d.ph) & 1) * 2 + (((ph & 1) + d.pw) & 1)];
-            if ((r = bwd_input_part(d, g[ph], cp.T, cp.ptr, cp.col, cp.src, w_vals, nnz, nks[ph], st))) return r;
+        for (int ph = 0; ph < 4; ++ph) {  // few input channels: the direct kernel per phase
+            const int a = ph >> 1, b = ph & 1;
+            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
+            ConvGeo<1> g = phase_geo(d, a, b, cp.tc);
+            g.G = dY;
+            g.Out = dX;
+            if ((r = bwd_input_part(d, g, cp.T, cp.ptr, cp.col, cp.src, w_vals, nnz, 1, st))) return r;
         }
         return SP_OK;
     }
@@ -1012,6 +1050,45 @@ extern "C" sp_status sp_conv_bwd_weight(const float *dY, const float *X, const s
     const int64_t pstride = spt2::part_stride(L.F);
     hipLaunchKernelGGL((spt2::k_sddmm2<ConvGeo<0>, true>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, g, L.F.view(),
                        (int)ntiles, sp2.nsplit, sp2.tps, part, pstride);
+    SP_CHECK_LAUNCH();
+    return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
+}
+
+extern "C" sp_status sp_conv_bwd(const float *dY, const float *X, const sp_conv_shape *s, const float *w_vals,
+                                 int64_t nnz, const void *plan, float *dX, float *dW, void *workspace,
+                                 size_t ws_bytes, void *stream) {
+    Dims d;
+    sp_status r = dims_of(s, nnz, d);
+    if (r) return r;
+    if (!plan || (d.B > 0 && (!dY || !dX)) || (nnz > 0 && (!w_vals || !dW)) || (d.B > 0 && nnz > 0 && !X))
+        return SP_ERR_INVALID_ARG;
+    if (!fits(d)) return SP_ERR_UNSUPPORTED;
+    size_t need;
+    sp_conv_bwd_weight_ws(s, nnz, &need);
+    if (need > 0 && (!workspace || ws_bytes < need)) return SP_ERR_WORKSPACE;
+    const bool fused = d.B > 0 && nnz > 0 && d.IC > FR_MAX &&
+                       ((d.sh == 1 && d.sw == 1) || (d.sh == 2 && d.sw == 2));
+    if (!fused) {  // the two passes one after the other on the stream
+        if ((r = sp_conv_bwd_input(dY, s, w_vals, nnz, plan, dX, stream))) return r;
+        return sp_conv_bwd_weight(dY, X, s, nnz, plan, dW, workspace, ws_bytes, stream);
+    }
+    hipStream_t st = (hipStream_t)stream;
+    ConvPlan L = plan_layout(plan, d, nnz);
+    PhaseSet ps;
+    bool split;
+    if ((r = input_grad_set(d, L, dY, dX, ps, split))) return r;
+    const int64_t ntiles = wgrad_tiles(d);
+    const spt2::Split sp2 = spt2::sddmm_split(L.F, ntiles);
+    const int64_t nB = L.F.P * L.F.K * sp2.nsplit;
+    if (ps.begin[4] + nB > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    if (split && (r = zero_launch(dX, d.B * d.IC * d.H * d.W, st))) return r;
+    ConvGeo<0> gw = make_geo<0>(d, true);
+    gw.G = X;
+    gw.D = dY;
+    float *part = (float *)workspace;
+    const int64_t pstride = spt2::part_stride(L.F);
+    hipLaunchKernelGGL(k_conv_bwd_fused, dim3((unsigned)(ps.begin[4] + nB)), dim3(spt2::NTHR), 0, st, ps, w_vals, gw,
+                       L.F.view(), (int)ntiles, sp2.tps, part, pstride, (int)nB);
     SP_CHECK_LAUNCH();
     return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
 }

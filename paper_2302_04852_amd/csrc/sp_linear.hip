@@ -460,18 +460,11 @@ __global__ __launch_bounds__(spt2::NTHR) __attribute__((amdgpu_waves_per_eu(4, 4
     int ntilesB, int tps, float *__restrict__ part, int64_t pstride, int nB) {
     __shared__ __attribute__((aligned(16))) float xs[spt2::XS_FLOATS];
     __shared__ spt2::SddmmLds sl;
-    const int total = nA + nB;
-    // XCD x runs blocks x, x+8, ...: cnt of them, the first cntp blocks of the
-    // XCD order (all XCDs before x) precede them.  Its share of the SDDMM
-    // items comes first, then its share of the SpMM items.
-    const int b = blockIdx.x, x = b % 8, kx = b / 8;
-    const int per = total / 8, rem = total % 8;
-    const int cntp = x * per + min(x, rem), cnt = per + (x < rem);
-    const int b0 = (int)((int64_t)cntp * nB / total), b1 = (int)((int64_t)(cntp + cnt) * nB / total);
-    if (kx < b1 - b0)
-        spt2::sddmm2_tile<GB, false>(gb, tvB, ntilesB, tps, part, pstride, b0 + kx, xs, sl);
+    int idx;
+    if (spt2::xcd_split2(blockIdx.x, nA, nB, idx))
+        spt2::sddmm2_tile<GB, false>(gb, tvB, ntilesB, tps, part, pstride, idx, xs, sl);
     else
-        spt2::spmm2_tile(ga, vals, tvA, ntilesA, 1, (cntp - b0) + (kx - (b1 - b0)), xs);
+        spt2::spmm2_tile(ga, vals, tvA, ntilesA, 1, idx, xs);
 }
 
 extern "C" sp_status sp_linear_bwd_input(const float *dY, int64_t B, int64_t in_f, int64_t out_f, const float *vals,

@@ -355,6 +355,25 @@ __device__ inline int64_t slot_block(int bs, int nb, int jb) { return (int64_t)(
 // SKIP: skip the slots past the last one with blocks in a round -- for
 // narrow layers, which fill only the first slots of every wave (it costs the
 // full-panel case a few percent, so full panels are compiled without it).
+// Block b of a grid running nA + nB work items of two products: XCD x runs
+// blocks x, x+8, ...; it gets a contiguous share of the B items followed by a
+// contiguous share of the A items (shares in proportion to its block count),
+// so each product keeps the XCD grouping of its own launch.  Returns true
+// with the B item index in idx, or false with the A item index.
+__device__ inline bool xcd_split2(int b, int nA, int nB, int &idx) {
+    const int total = nA + nB;
+    const int x = b % 8, kx = b / 8;
+    const int per = total / 8, rem = total % 8;
+    const int cntp = x * per + min(x, rem), cnt = per + (x < rem);
+    const int b0 = (int)((int64_t)cntp * nB / total), b1 = (int)((int64_t)(cntp + cnt) * nB / total);
+    if (kx < b1 - b0) {
+        idx = b0 + kx;
+        return true;
+    }
+    idx = (cntp - b0) + (kx - (b1 - b0));
+    return false;
+}
+
 // LDS of one SDDMM workgroup beyond the staged chunk.
 struct SddmmLds {
     float dsx[NW * NG * T];  // per-wave D transpose scratch

@@ -107,6 +107,18 @@ class GpuConv:
         return dW[:self.nnz]
 
 
+    def bwd(self, dY, X):
+        """Both gradients from sp_conv_bwd."""
+        import torch
+        B, IC, H, Wd = self.dims[:4]
+        ws = torch.empty(max(self.sp.sp_conv_bwd_weight_ws(self.shape, self.nnz), 1), dtype=torch.uint8,
+                         device="cuda")
+        dX = torch.full((B, IC, H, Wd), float("nan"), device="cuda")
+        dW = torch.full((max(self.nnz, 1),), float("nan"), device="cuda")
+        self.sp.sp_conv_bwd(dY, X, self.shape, self.w_vals, self.nnz, self.plan, dX, dW, ws)
+        return dX, dW[:self.nnz]
+
+
 def _oracle_shape(orc, dims, B=None):
     b, IC, H, Wd, OC, KH, KW, stride, pad = dims
     return orc.conv_shape(b if B is None else B, IC, H, Wd, OC, KH, KW, stride, pad)
@@ -137,6 +149,11 @@ def _run_all(sp, orc, d, dims, name, sample_images=None):
     assert_parity(dX.cpu().numpy()[imgs], dXr, dXa, name + " bwd_input")
     dWr, dWa = orc.conv_bwd_weight(d["dY"], d["X"], L.oshape, o_oc, o_ic, o_x, o_y)
     assert_parity(dW.cpu().numpy(), dWr, dWa, name + " bwd_weight")
+    # both gradients in one call: the same kernels and splits, so the same bits
+    dXf, dWf = L.bwd(dYd, Xd)
+    torch.cuda.synchronize()
+    assert torch.equal(dXf, dX), name + " sp_conv_bwd dX differs from sp_conv_bwd_input"
+    assert torch.equal(dWf, dW), name + " sp_conv_bwd dW differs from sp_conv_bwd_weight"
     return L, Y, dX, dW
 
 
