@@ -34,7 +34,9 @@ namespace {
 constexpr int OOB = 0x7ffffff0;       // byte offset beyond any accepted buffer range
 constexpr int TOK_INVALID = -(1 << 28);  // spatial origin of tokens past the end
 constexpr int64_t MAX_BYTES = 0x7fff0000LL;
-// The staging's multiply-high divisions n / d (d <= 32) are exact for n < 2^26.
+// The staging's multiply-high divisions n / d (d <= 64) are exact for n < 2^25
+// (columns beyond that exist only past the last one, where the result is not
+// used).
 constexpr int TABLE_MAX_COLS = 1 << 25;
 
 // --------------------------------------------------------------------------
@@ -221,10 +223,11 @@ struct ConvGeo {
         int a, c;      // spatial origin of the token (see tile_init)
         uint32_t gbase4;  // byte offset of that origin in G (modulo 2^32)
         int obase;     // element offset of the token's output pixel in channel 0, -1 past the end
-        // DIR 0/1, KK <= 32: (bad_hi:bad) has bit j set where tap j mod KK
-        // (tap x*KW + y) is outside G -- the tap mask repeated, so that bits
-        // t..t+31 describe 32 consecutive columns starting at tap t.
-        uint32_t bad, bad_hi;
+        // DIR 0/1, KK <= 64: bit j of the 128-bit bad[3]:..:bad[0] is set
+        // where tap j mod KK (tap x*KW + y) is outside G -- the tap mask
+        // repeated, so that bits t..t+31 (t < 64) describe 32 consecutive
+        // columns starting at tap t.
+        uint32_t bad[4];
         uint32_t dbase4;  // byte offset of obase in D, 2^31 (past any buffer range) past the end
     };
 
@@ -253,8 +256,9 @@ struct ConvGeo {
         // Valid taps form a rectangle x in [x0, x1), y in [y0, y1) (empty past
         // the end).  KK >= 1 keeps the doubling loop finite (an empty tap
         // class has no columns and never stages).
-        uint64_t bad = ~0ull;
-        if (DIR != 2 && KK >= 1 && KK <= 32 && t < ntok) {
+        uint64_t blo = ~0ull, bhi = ~0ull;
+        if (DIR != 2 && KK >= 1 && KK <= 64 && t < ntok) {
+            uint64_t bad = ~0ull;
             int x0, x1, y0, y1;
             if (DIR == 0) {  // 0 <= a + x < gH
                 x0 = max(0, -tk.a), x1 = min(KH, gH - tk.a);
@@ -264,27 +268,37 @@ struct ConvGeo {
                 y0 = max(0, tk.c - gW + 1), y1 = min(KW, tk.c + 1);
             }
             if (y0 < y1) {
-                const uint64_t ym = ((1ull << (y1 - y0)) - 1ull) << y0;
+                const uint64_t ym = ((y1 - y0 == 64) ? ~0ull : ((1ull << (y1 - y0)) - 1ull)) << y0;
                 for (int x = x0; x < x1; ++x) bad &= ~(ym << (x * KW));
             }
-            bad &= (1ull << KK) - 1ull;
-            for (int len = KK; len < 64; len *= 2) bad |= bad << len;
+            if (KK < 64) bad &= (1ull << KK) - 1ull;
+            // repeat with period KK over 128 bits (hi:lo), doubling the length
+            blo = bad;
+            bhi = 0;
+            for (int len = KK; len < 128; len *= 2) {
+                const uint64_t shi = len >= 64 ? blo << (len - 64) : (bhi << len) | (blo >> (64 - len));
+                const uint64_t slo = len >= 64 ? 0ull : blo << len;
+                blo |= slo;
+                bhi |= shi;
+            }
         }
-        tk.bad = (uint32_t)bad;
-        tk.bad_hi = (uint32_t)(bad >> 32);
+        tk.bad[0] = (uint32_t)blo;
+        tk.bad[1] = (uint32_t)(blo >> 32);
+        tk.bad[2] = (uint32_t)bhi;
+        tk.bad[3] = (uint32_t)(bhi >> 32);
     }
 
     // Byte offsets of the wave's CPW columns for this thread's token, past the
     // buffer range where the element is outside G, past the last column or
     // past the last token.  The loads are issued afterwards from one place.
     //
-    // Table path (DIR 0/1, KK <= 32, all CPW columns valid): lane l of each
-    // 16-lane row computes the column offsets of columns cb + l and
-    // cb + 16 + l once; element i takes its offset from lane i & 15 by DPP,
-    // folded into the add, and bit 31 from bit i of the token's repeated tap
-    // mask shifted by the first column's tap, which lifts the offset past the
-    // buffer range (every valid offset is below 2^31).  3 VALU per element
-    // and no per-element scalar bookkeeping.
+    // Table path (DIR 0/1, KK <= 64): lane l of each 16-lane row computes the
+    // column offsets of columns cb + l and cb + 16 + l once; element i takes
+    // its offset from lane i & 15 by DPP, folded into the add, and bit 31 from
+    // bit i of the token's repeated tap mask shifted by the first column's
+    // tap (columns past the last get their bit set too), which lifts the
+    // offset past the buffer range (every valid offset is below 2^31).
+    // 3 VALU per element and no per-element scalar bookkeeping.
     __device__ void offsets_table(uint32_t (&o)[spt2::PF], const Tok &tk, int cb, int t0) const {
         const int l = threadIdx.x & 15;
         int tab[2];
@@ -298,7 +312,11 @@ struct ConvGeo {
             const int cofs = DIR == 0 ? (int)(c * gplane + xx * gW + yy) : (int)(c * gplane) - (int)(xx * gW + yy);
             tab[h] = cofs * 4;
         }
-        const uint32_t B = (uint32_t)((((uint64_t)tk.bad_hi << 32) | tk.bad) >> t0);
+        // bits t0..t0+31 of the repeated mask (t0 < 64), and the columns past
+        // the last marked outside
+        const bool w1 = t0 >= 32;
+        uint32_t B = __builtin_amdgcn_alignbit(w1 ? tk.bad[2] : tk.bad[1], w1 ? tk.bad[1] : tk.bad[0], t0 & 31);
+        if (ncols - cb < CPW) B |= ~0u << (ncols - cb);
         offsets_table_at<0>(o, tk, tab, B);
     }
     template <int I>
@@ -352,7 +370,7 @@ struct ConvGeo {
             return 0xffffffffu;
         }
         uint32_t o[spt2::PF];
-        if (DIR != 2 && KK <= 32 && ncols <= TABLE_MAX_COLS && cb + CPW <= ncols)
+        if (DIR != 2 && KK <= 64 && ncols <= TABLE_MAX_COLS)
             offsets_table(o, tk, cb, cb % KK);
         else
             offsets_walk(o, tk, cb);
@@ -813,11 +831,13 @@ int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, spt2
 // and stride 1 (one part: the input-channel-major tiling) or 2 (the four
 // phases over their tap classes).  Stride 1 splits its chunks as the
 // single-product launch does, stride 2 on the total items of its phases, so
-// either kind of launch computes the same sums.  split: dX must be zero-filled
-// first.
-sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, float *dX, PhaseSet &ps, bool &split) {
+// either kind of launch computes the same sums.  A phase whose tap class is
+// empty (1x1 stride-2 layers: three of the four) gets no items: its pixels
+// are zero.  zero: dX must be zero-filled first (a split phase adds into it,
+// or an empty phase leaves its pixels to the fill).
+sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, float *dX, PhaseSet &ps, bool &zero) {
     int64_t items = 0;
-    split = false;
+    zero = false;
     if (d.sh == 1 && d.sw == 1) {
         ConvGeo<1> g = make_geo<1>(d, false);
         g.G = dY;
@@ -837,6 +857,10 @@ sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, floa
             ps.g[ph].Out = dX;
             ps.tv[ph] = cp.T.view();
             ps.ntiles[ph] = (int)sp::ceil_div(ps.g[ph].ntok, spt2::T);
+            if (cp.T.K == 0 && ps.ntiles[ph] > 0) {
+                zero = true;
+                ps.ntiles[ph] = 0;
+            }
             items += cp.T.P * ps.ntiles[ph];
         }
         for (int ph = 0; ph < 4; ++ph) ps.nks[ph] = (items < NUM_CU && ps.tv[ph].K >= 2) ? 2 : 1;
@@ -845,7 +869,7 @@ sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, floa
     for (int ph = 0; ph < 4; ++ph) {
         ps.begin[ph] = (int)total;
         total += (int64_t)ps.tv[ph].P * ps.ntiles[ph] * ps.nks[ph];
-        split |= ps.nks[ph] > 1 && ps.ntiles[ph] > 0;
+        zero |= ps.nks[ph] > 1 && ps.ntiles[ph] > 0;
         if (total > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     }
     ps.begin[4] = (int)total;
