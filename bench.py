@@ -31,7 +31,9 @@ step time and `value`.
 Prints ONE JSON line.  Extra fields: `roofline` (dominant kernel: algorithmic
 bytes / FLOPs per launch over its event-timed duration), `cpu_baseline` (the
 CPU oracle timed on the host over a bounded sample, about 10 s), `ops`
-(per-op times).
+(per-op times, warm caches: consecutive steps), `cold` (per-op medians with
+the caches evicted before every launch, and the achievable HBM rate of a
+1 GiB copy).
 """
 from __future__ import annotations
 
@@ -61,6 +63,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", choices=WORKLOADS, default="ffn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cold-reps", type=int, default=10,
+                    help="launches per op for the cold-cache per-op medians (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle baseline (whole sample passes are repeated)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -70,6 +74,7 @@ def parse():
 
 COPY_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm2_k_bwd_fused_ffn_pair_hbm_traffic.txt")
+FLUSH_BYTES = 1 << 30
 KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", "sp_linear.hip"]
 
 
@@ -268,6 +273,57 @@ def time_ops(torch, ops, steps, warmup):
     return e0.elapsed_time(e1) / steps, [t / steps for t in per_op], ms_instr
 
 
+def cold_ops(torch, ops, reps):
+    """Per-op times with cold caches: before every timed launch a 1 GiB fill
+    (more than the L2s and the 256 MB last-level cache together) evicts the
+    operands.  Median over `reps` launches of each op."""
+    scratch = torch.empty(FLUSH_BYTES // 4, device="cuda")
+    stream = torch.cuda.current_stream()
+    evs = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+           for _ in ops]
+    for op, ev in zip(ops, evs):
+        for a, b in ev:
+            scratch.fill_(1.0)
+            a.record(stream)
+            op[1]()
+            b.record(stream)
+    torch.cuda.synchronize()
+    return [float(np.median([a.elapsed_time(b) for a, b in ev])) for ev in evs]
+
+
+def copy_rate_GBps(torch):
+    """Achievable HBM rate: a 1 GiB device-to-device copy (read + write
+    counted), best of 5."""
+    a = torch.ones(FLUSH_BYTES // 4, device="cuda")
+    b = torch.empty_like(a)
+    stream = torch.cuda.current_stream()
+    best = None
+    for _ in range(5):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        b.copy_(a)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        best = ms if best is None else min(best, ms)
+    return 2.0 * FLUSH_BYTES / (best * 1e-3) / 1e9
+
+
+def cold_record(torch, args, ops):
+    """Cold-cache per-op medians and the achievable HBM rate, or None."""
+    if args.cold_reps <= 0:
+        return None
+    t = cold_ops(torch, ops, args.cold_reps)
+    rate = copy_rate_GBps(torch)
+    return {"method": "median of %d launches per op, each after a 1 GiB fill that evicts L2 and the "
+                      "last-level cache" % args.cold_reps,
+            "hbm_copy_GBps": round(rate, 1),
+            "step_ms": round(sum(t), 5),
+            "ops": {o[0]: dict(op_row(ms, o[3], o[4]), hbm_frac_of_copy=round(o[4] / (ms * 1e-3) / 1e9 / rate, 4))
+                    for o, ms in zip(ops, t)}}
+
+
 def op_row(ms, fl, by):
     return {"ms": round(ms, 5), "tflops": round(fl / ms / 1e9, 3), "alg_GBps": round(by / ms / 1e6, 1),
             "hbm_frac": round(by / ms / 1e6 / HBM_PEAK_GBS, 4), "bound": bound_of(fl, by)}
@@ -391,6 +447,9 @@ def run_linear(args, sp, torch, which):
     out["ms_per_step_with_op_events"] = round(ms_instr, 5)
     out["roofline"] = roofline(dom, kind, fl, by, dom_ms, traffic, {"source_hash": kernel_source_hash()})
     out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    cold = cold_record(torch, args, ops)
+    if cold:
+        out["cold"] = cold
     out["plan_ms"] = {L.name: round(L.plan_ms, 3) for L in layers}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_linear(layers_np, args.cpu_seconds, which)
@@ -467,6 +526,9 @@ def run_conv(args, sp, torch, which):
                         "alg_GBps": round(v[2] / v[0] / 1e6, 1), "bound": bound_of(v[1], v[2])}
                     for k, v in kinds.items()}
     out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    cold = cold_record(torch, args, ops)
+    if cold:
+        out["cold"] = cold
     out["plan_ms"] = {L.name: round(L.plan_ms, 3) for L in layers}
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline_conv(layers, args.cpu_seconds)

@@ -791,16 +791,12 @@ sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, c
     return SP_OK;
 }
 
-// Input gradient of one unit-stride problem (the whole layer at stride 1, or
-// one phase of a stride-2 layer) over a CSR by input channel and its tiling.
-// nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
-// nnz bounds the entries of the part (the direct kernel's LDS size).
 // The four phases of a stride-2 input gradient as one launch: the phases of
 // small layers have a few dozen token tiles each, far too few for the chip
 // when launched one after another.  Block b runs work item b - begin[ph] of
 // the phase whose range [begin[ph], begin[ph+1]) holds b.  Blocks are not
 // regrouped by XCD: consecutive blocks go to different XCDs, so each XCD gets
-// its share of every phase (phases with no taps only write zeros).
+// its share of every phase.
 struct PhaseSet {
     ConvGeo<1> g[4];
     spt2::SlotView tv[4];
@@ -817,6 +813,10 @@ __global__ __launch_bounds__(spt2::NTHR) void k_spmm2_phases(PhaseSet ps, const 
     spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph], xs);
 }
 
+// Input gradient of one unit-stride problem (the whole layer at stride 1, or
+// one phase of a stride-2 layer) over a CSR by input channel and its tiling.
+// nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
+// nnz bounds the entries of the part (the direct kernel's LDS size).
 sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,
                          const int32_t *col, const int32_t *src, const float *vals, int64_t nnz, int nks,
                          hipStream_t st) {

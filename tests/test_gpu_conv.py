@@ -356,6 +356,14 @@ def test_error_paths(sp, orc):
     with pytest.raises(sp.SparsePropError) as e:
         sp.sp_conv_plan(L.shape, L.w_oc, L.w_ic, L.w_x, L.w_y, L.nnz, small)
     assert e.value.status == sp.SP_ERR_WORKSPACE
+    dX = torch.empty(2, 4, 8, 8, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_conv_bwd(dY, X, L.shape, L.w_vals, L.nnz, L.plan, dX, dW, small)
+    assert e.value.status == sp.SP_ERR_WORKSPACE
+    ws = torch.empty(sp.sp_conv_bwd_weight_ws(L.shape, L.nnz), dtype=torch.uint8, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_conv_bwd(dY, X, L.shape, L.w_vals, L.nnz, L.plan, None, dW, ws)
+    assert e.value.status == sp.SP_ERR_INVALID_ARG
 
 
 def test_validate_host(sp, orc):

@@ -244,6 +244,14 @@ def test_error_paths(sp, orc):
     with pytest.raises(sp.SparsePropError) as e:
         sp.sp_linear_plan(16, 32, L.row_ptr, L.col_idx, L.nnz, small)
     assert e.value.status == sp.SP_ERR_WORKSPACE
+    dX = torch.empty(8, 16, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_bwd(dY, X, 8, 16, 32, L.vals, L.nnz, L.plan, dX, dW, small)
+    assert e.value.status == sp.SP_ERR_WORKSPACE
+    ws = torch.empty(sp.sp_linear_bwd_weight_ws(8, 16, 32, L.nnz), dtype=torch.uint8, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_bwd(dY, X, 8, 16, 32, L.vals, L.nnz, L.plan, None, dW, ws)
+    assert e.value.status == sp.SP_ERR_INVALID_ARG
 
 
 @pytest.mark.parametrize("layer", [0, 1])
