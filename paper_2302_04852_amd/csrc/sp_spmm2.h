@@ -25,7 +25,7 @@
 // 512-byte load per block -- and gathers its value; iteration i of group g
 // then broadcasts lane i of the group's 16-lane row to the whole group with
 // DPP row_newbcast.  The metadata and values are requested a slot or two
-// ahead of their use (see k_spmm2).
+// ahead of their use (see spmm2_tile).
 #pragma once
 
 #include "sp_common.h"
@@ -350,11 +350,6 @@ __device__ inline float dot4(const float (&d)[4], const float4 &x) {
 // is never used.
 __device__ inline int64_t slot_block(int bs, int nb, int jb) { return (int64_t)(bs + min(jb, nb)) * BLK; }
 
-// Geometry addition for the SDDMM:
-//   float4 load_dq(tok, t0, row0, s)   D[t0 + lane][rows of slot s of groups 0..3 of this wave]
-// SKIP: skip the slots past the last one with blocks in a round -- for
-// narrow layers, which fill only the first slots of every wave (it costs the
-// full-panel case a few percent, so full panels are compiled without it).
 // Block b of a grid running nA + nB work items of two products: XCD x runs
 // blocks x, x+8, ...; it gets a contiguous share of the B items followed by a
 // contiguous share of the A items (shares in proportion to its block count),
@@ -380,6 +375,11 @@ struct SddmmLds {
     int rounds[NW];
 };
 
+// Geometry addition for the SDDMM:
+//   float4 load_dq(tok, t0, row0, s)   D[t0 + lane][rows of slot s of groups 0..3 of this wave]
+// SKIP: skip the slots past the last one with blocks in a round -- for
+// narrow layers, which fill only the first slots of every wave (it costs the
+// full-panel case a few percent, so full panels are compiled without it).
 // Work item L in [0, P*K*nsplit): one (panel, chunk) and token range L / (P*K).
 template <class Geo, bool SKIP>
 __device__ void sddmm2_tile(const Geo &geo, const SlotView &tv, int ntiles, int tps, float *__restrict__ part,
