@@ -716,12 +716,26 @@ constexpr int FR_ENT = 2048;  // entries staged per round (at most 32 KB)
 
 // Dynamic LDS: min(entries, FR_ENT) * 16 bytes, so that small stems leave
 // room for more workgroups per compute unit.
-__global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__restrict__ ptr,
-                                                 const int32_t *__restrict__ col, const int32_t *__restrict__ src,
-                                                 const float *__restrict__ vals, int nrows) {
+// The parts (the whole layer at stride 1, the four phases at stride 2) run
+// as one launch: block b takes block b - begin[p] of the part p whose range
+// holds b, so the last round of blocks is shared by all parts.
+struct FewSet {
+    ConvGeo<1> g[4];
+    const int32_t *ptr[4], *col[4], *src[4];
+    int begin[5];
+};
+
+__global__ __launch_bounds__(256) void k_fewrows(FewSet fs, const float *__restrict__ vals, int nrows) {
     extern __shared__ int4 ent[];
+    int part = 0;
+#pragma unroll
+    for (int i = 1; i < 4; ++i) part += (int)blockIdx.x >= fs.begin[i];
+    const ConvGeo<1> &g = fs.g[part];
+    const int32_t *__restrict__ ptr = fs.ptr[part];
+    const int32_t *__restrict__ col = fs.col[part];
+    const int32_t *__restrict__ src = fs.src[part];
     const int tid = threadIdx.x;
-    const int t = (int)blockIdx.x * 256 + tid;
+    const int t = ((int)blockIdx.x - fs.begin[part]) * 256 + tid;
     int a = TOK_INVALID, c = TOK_INVALID, gbase = 0, obase = -1;
     if (t < g.ntok) {
         const int b = t / g.npix, pix = t - b * g.npix;
@@ -781,12 +795,39 @@ __global__ __launch_bounds__(256) void k_fewrows(ConvGeo<1> g, const int32_t *__
     }
 }
 
-sp_status fewrows(const ConvGeo<1> &g, const int32_t *ptr, const int32_t *col, const int32_t *src, const float *vals,
-                  int nrows, int64_t nent, hipStream_t st) {
-    if (g.ntok == 0) return SP_OK;
-    const size_t lds = (size_t)std::max<int64_t>(1, std::min<int64_t>(nent, FR_ENT)) * sizeof(int4);
-    hipLaunchKernelGGL(k_fewrows, dim3((unsigned)sp::ceil_div(g.ntok, 256)), dim3(256), lds, st, g, ptr, col, src,
-                       vals, nrows);
+// Direct input gradient of a layer with at most FR_MAX input channels and
+// stride 1 or 2: one launch over its parts.  nnz bounds the entries of a part
+// (the LDS size).
+sp_status fewrows_layer(const Dims &d, const ConvPlan &L, const float *dY, float *dX, const float *vals, int64_t nnz,
+                        hipStream_t st) {
+    FewSet fs;
+    int64_t total = 0;
+    for (int p = 0; p < 4; ++p) {
+        ConvGeo<1> g;
+        if (d.sh == 1) {
+            g = make_geo<1>(d, false);
+            fs.ptr[p] = L.t_ic_ptr;
+            fs.col[p] = L.colB;
+            fs.src[p] = L.t_perm;
+        } else {
+            const int a = p >> 1, b = p & 1;
+            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
+            g = phase_geo(d, a, b, cp.tc);
+            fs.ptr[p] = cp.ptr;
+            fs.col[p] = cp.col;
+            fs.src[p] = cp.src;
+        }
+        g.G = dY;
+        g.Out = dX;
+        fs.g[p] = g;
+        fs.begin[p] = (int)total;
+        if (d.sh == 2 || p == 0) total += sp::ceil_div(g.ntok, 256);
+        if (total > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    }
+    fs.begin[4] = (int)total;
+    if (total == 0) return SP_OK;
+    const size_t lds = (size_t)std::max<int64_t>(1, std::min<int64_t>(nnz, FR_ENT)) * sizeof(int4);
+    hipLaunchKernelGGL(k_fewrows, dim3((unsigned)total), dim3(256), lds, st, fs, vals, (int)d.IC);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
@@ -813,17 +854,6 @@ __global__ __launch_bounds__(spt2::NTHR) void k_spmm2_phases(PhaseSet ps, const 
     spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph], xs);
 }
 
-// Input gradient of one unit-stride problem (the whole layer at stride 1, or
-// one phase of a stride-2 layer) over a CSR by input channel and its tiling.
-// nks: slab splits of the tiled path (its output zero-filled beforehand when 2).
-// nnz bounds the entries of the part (the direct kernel's LDS size).
-sp_status bwd_input_part(const Dims &d, const ConvGeo<1> &g, const spt2::SlotTiling &t, const int32_t *ptr,
-                         const int32_t *col, const int32_t *src, const float *vals, int64_t nnz, int nks,
-                         hipStream_t st) {
-    if (g.ntok == 0) return SP_OK;
-    if (d.IC <= FR_MAX) return fewrows(g, ptr, col, src, vals, (int)d.IC, nnz, st);
-    return spmm(t, g, vals, nks, st);
-}
 
 int64_t wgrad_tiles(const Dims &d) { return sp::ceil_div(d.B * d.OH * d.OW, spt2::T); }
 
@@ -997,35 +1027,24 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
     if (nnz == 0) return zero_launch(dX, d.B * d.IC * d.H * d.W, st);
     ConvPlan L = plan_layout(plan, d, nnz);
     const int64_t nout = d.B * d.IC * d.H * d.W;
-    if (d.sh == 1 && d.sw == 1) {
+    const bool s1 = d.sh == 1 && d.sw == 1, s2 = d.sh == 2 && d.sw == 2;
+    if (d.IC <= FR_MAX && (s1 || s2)) return fewrows_layer(d, L, dY, dX, w_vals, nnz, st);
+    if (s1) {
         ConvGeo<1> g = make_geo<1>(d, false);
         g.G = dY;
         g.Out = dX;
-        const int nks = d.IC <= FR_MAX ? 1 : spmm_splits(L.G, g.ntok);
+        const int nks = spmm_splits(L.G, g.ntok);
         if (nks > 1 && (r = zero_launch(dX, nout, st))) return r;
-        return bwd_input_part(d, g, L.G, L.t_ic_ptr, L.colB, L.t_perm, w_vals, nnz, nks, st);
+        return spmm(L.G, g, w_vals, nks, st);
     }
-    if (d.sh == 2 && d.sw == 2) {  // four phases, each over its tap class
-        if (d.IC > FR_MAX) {
-            // One launch over the four phases; the chunk split is decided on
-            // the total number of work items.
-            PhaseSet ps;
-            bool split;
-            if ((r = input_grad_set(d, L, dY, dX, ps, split))) return r;
-            if (split && (r = zero_launch(dX, nout, st))) return r;
-            if (ps.begin[4] == 0) return SP_OK;
-            hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
-            SP_CHECK_LAUNCH();
-            return SP_OK;
-        }
-        for (int ph = 0; ph < 4; ++ph) {  // few input channels: the direct kernel per phase
-            const int a = ph >> 1, b = ph & 1;
-            const ClassPart &cp = L.cls[((a + d.ph) & 1) * 2 + ((b + d.pw) & 1)];
-            ConvGeo<1> g = phase_geo(d, a, b, cp.tc);
-            g.G = dY;
-            g.Out = dX;
-            if ((r = bwd_input_part(d, g, cp.T, cp.ptr, cp.col, cp.src, w_vals, nnz, 1, st))) return r;
-        }
+    if (s2) {  // one launch over the four phases, each over its tap class
+        PhaseSet ps;
+        bool zero;
+        if ((r = input_grad_set(d, L, dY, dX, ps, zero))) return r;
+        if (zero && (r = zero_launch(dX, nout, st))) return r;
+        if (ps.begin[4] == 0) return SP_OK;
+        hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
+        SP_CHECK_LAUNCH();
         return SP_OK;
     }
     ConvGeo<2> g = make_geo<2>(d, false);
