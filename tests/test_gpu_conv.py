@@ -273,6 +273,8 @@ def test_empty_pattern_and_empty_batch(sp, orc):
     assert torch.all(L.fwd(X) == 0)
     assert torch.all(L.bwd_input(dY) == 0)
     assert L.bwd_weight(dY, X).numel() == 0
+    dXf, dWf = L.bwd(dY, X)
+    assert torch.all(dXf == 0) and dWf.numel() == 0
     # an empty batch is a no-op for every pass
     d, dims = _layer(orc, 7200, 2, 4, 7, 7, 6, 3, 3, (1, 1), (1, 1), 0.5)
     L = GpuConv(sp, orc, d["mask"], d["W"], 0, 7, 7, (1, 1), (1, 1))
@@ -281,6 +283,9 @@ def test_empty_pattern_and_empty_batch(sp, orc):
     sp.sp_conv_bwd_input(e, L.shape, L.w_vals, L.nnz, L.plan, e)
     dW = torch.full((L.nnz,), 5.0, device="cuda")
     sp.sp_conv_bwd_weight(e, e, L.shape, L.nnz, L.plan, dW, None)
+    assert torch.all(dW == 0)
+    dW.fill_(5.0)
+    sp.sp_conv_bwd(e, e, L.shape, L.w_vals, L.nnz, L.plan, e, dW, None)
     assert torch.all(dW == 0)
 
 
@@ -326,8 +331,8 @@ def test_deterministic(sp, orc):
     L = GpuConv(sp, orc, d["mask"], d["W"], dims[0], dims[2], dims[3], dims[7], dims[8])
     X = torch.from_numpy(d["X"]).cuda()
     dY = torch.from_numpy(d["dY"]).cuda()
-    a = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
-    b = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
+    a = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X)) + L.bwd(dY, X)
+    b = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X)) + L.bwd(dY, X)
     for u, v in zip(a, b):
         assert torch.equal(u, v)
 

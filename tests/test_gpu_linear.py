@@ -213,6 +213,8 @@ def test_empty_pattern_writes_zeros(sp, orc):
     assert torch.all(L.fwd(X) == 0)
     assert torch.all(L.bwd_input(dY) == 0)
     assert L.bwd_weight(dY, X).numel() == 0
+    dXf, dWf = L.bwd(dY, X)
+    assert torch.all(dXf == 0) and dWf.numel() == 0
 
 
 def test_deterministic(sp, orc):
@@ -221,8 +223,8 @@ def test_deterministic(sp, orc):
     L = GpuLayer(sp, orc, d["mask"], d["W"])
     X = torch.from_numpy(d["X"]).cuda()
     dY = torch.from_numpy(d["dY"]).cuda()
-    a = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
-    b = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X))
+    a = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X)) + L.bwd(dY, X)
+    b = (L.fwd(X), L.bwd_input(dY), L.bwd_weight(dY, X)) + L.bwd(dY, X)
     for u, v in zip(a, b):
         assert torch.equal(u, v)
 
