@@ -389,12 +389,13 @@ struct ConvGeo {
     // Accumulators -> output through LDS: ys[position][64 tokens], then thread
     // tid writes token tid & 63 of rows (tid >> 6) + 8j: runs of consecutive
     // pixels of one channel.
-    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &tk, int64_t, int64_t row0,
+    template <int NSA>
+    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &tk, int64_t, int64_t row0,
                           bool add) const {
         const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
         __syncthreads();
 #pragma unroll
-        for (int s = 0; s < spt2::NS; ++s) {
+        for (int s = 0; s < NSA; ++s) {
             const int pos = spt2::NG * spt2::NW * s + spt2::NG * w + g;
 #pragma unroll
             for (int k = 0; k < 4; ++k) ys[pos * spt2::YS + 4 * gl + k] = acc[s][k];
@@ -683,14 +684,29 @@ int spmm_splits(const spt2::SlotTiling &t, int64_t ntok) {
 }
 
 // The output must hold zeros where nks == 2.
+// Slots a SpMM over tiling t has to process: a single panel of at most 64
+// or 128 rows fills only the first 2 or 4 slots of every wave.
+int active_slots(const spt2::SlotTiling &t) {
+    if (t.P != 1) return spt2::NS;
+    return t.rows <= 2 * spt2::NG * spt2::NW ? 2 : t.rows <= 4 * spt2::NG * spt2::NW ? 4 : spt2::NS;
+}
+
 template <class Geo>
 sp_status spmm(const spt2::SlotTiling &t, const Geo &geo, const float *vals, int nks, hipStream_t st) {
     const int64_t ntiles = sp::ceil_div(geo.ntok, spt2::T);
     const int64_t nwg = t.P * ntiles * nks;
     if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
     if (nwg == 0) return SP_OK;
-    hipLaunchKernelGGL((spt2::k_spmm2<Geo>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals, t.view(),
-                       (int)ntiles, nks);
+    const int nsa = active_slots(t);
+    if (nsa == 2)
+        hipLaunchKernelGGL((spt2::k_spmm2<Geo, 2>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals,
+                           t.view(), (int)ntiles, nks);
+    else if (nsa == 4)
+        hipLaunchKernelGGL((spt2::k_spmm2<Geo, 4>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals,
+                           t.view(), (int)ntiles, nks);
+    else
+        hipLaunchKernelGGL((spt2::k_spmm2<Geo>), dim3((unsigned)nwg), dim3(spt2::NTHR), 0, st, geo, vals, t.view(),
+                           (int)ntiles, nks);
     SP_CHECK_LAUNCH();
     return SP_OK;
 }
@@ -845,13 +861,14 @@ struct PhaseSet {
     int begin[5];
 };
 
+template <int NSA>
 __global__ __launch_bounds__(spt2::NTHR) void k_spmm2_phases(PhaseSet ps, const float *__restrict__ vals) {
     const int L = blockIdx.x;
     int ph = 0;
 #pragma unroll
     for (int i = 1; i < 4; ++i) ph += L >= ps.begin[i];
     __shared__ __attribute__((aligned(16))) float xs[spt2::XS_FLOATS];
-    spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph], xs);
+    spt2::spmm2_tile<ConvGeo<1>, NSA>(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], L - ps.begin[ph], xs);
 }
 
 
@@ -911,6 +928,7 @@ sp_status input_grad_set(const Dims &d, const ConvPlan &L, const float *dY, floa
 // set share the grid (each XCD runs its share of the SDDMM items first, then
 // of the SpMM items), so workgroups of both kinds on a compute unit hide part
 // of each other's staging and metadata latency.
+template <int NSA>
 __global__ __launch_bounds__(spt2::NTHR) __attribute__((amdgpu_waves_per_eu(4, 4))) void k_conv_bwd_fused(
     PhaseSet ps, const float *__restrict__ vals, ConvGeo<0> gw, spt2::SlotView tvF, int ntilesW, int tps,
     float *__restrict__ part, int64_t pstride, int nB) {
@@ -923,7 +941,7 @@ __global__ __launch_bounds__(spt2::NTHR) __attribute__((amdgpu_waves_per_eu(4, 4
         int ph = 0;
 #pragma unroll
         for (int i = 1; i < 4; ++i) ph += idx >= ps.begin[i];
-        spt2::spmm2_tile(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], idx - ps.begin[ph], xs);
+        spt2::spmm2_tile<ConvGeo<1>, NSA>(ps.g[ph], vals, ps.tv[ph], ps.ntiles[ph], ps.nks[ph], idx - ps.begin[ph], xs);
     }
 }
 
@@ -1043,7 +1061,14 @@ extern "C" sp_status sp_conv_bwd_input(const float *dY, const sp_conv_shape *s, 
         if ((r = input_grad_set(d, L, dY, dX, ps, zero))) return r;
         if (zero && (r = zero_launch(dX, nout, st))) return r;
         if (ps.begin[4] == 0) return SP_OK;
-        hipLaunchKernelGGL(k_spmm2_phases, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
+        const int nsa = active_slots(L.cls[0].T);
+        if (nsa == 2)
+            hipLaunchKernelGGL(k_spmm2_phases<2>, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
+        else if (nsa == 4)
+            hipLaunchKernelGGL(k_spmm2_phases<4>, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps, w_vals);
+        else
+            hipLaunchKernelGGL(k_spmm2_phases<spt2::NS>, dim3((unsigned)ps.begin[4]), dim3(spt2::NTHR), 0, st, ps,
+                               w_vals);
         SP_CHECK_LAUNCH();
         return SP_OK;
     }
@@ -1130,8 +1155,16 @@ extern "C" sp_status sp_conv_bwd(const float *dY, const float *X, const sp_conv_
     gw.D = dY;
     float *part = (float *)workspace;
     const int64_t pstride = spt2::part_stride(L.F);
-    hipLaunchKernelGGL(k_conv_bwd_fused, dim3((unsigned)(ps.begin[4] + nB)), dim3(spt2::NTHR), 0, st, ps, w_vals, gw,
-                       L.F.view(), (int)ntiles, sp2.tps, part, pstride, (int)nB);
+    const int nsa = d.sh == 1 ? active_slots(L.G) : active_slots(L.cls[0].T);
+    if (nsa == 2)
+        hipLaunchKernelGGL(k_conv_bwd_fused<2>, dim3((unsigned)(ps.begin[4] + nB)), dim3(spt2::NTHR), 0, st, ps,
+                           w_vals, gw, L.F.view(), (int)ntiles, sp2.tps, part, pstride, (int)nB);
+    else if (nsa == 4)
+        hipLaunchKernelGGL(k_conv_bwd_fused<4>, dim3((unsigned)(ps.begin[4] + nB)), dim3(spt2::NTHR), 0, st, ps,
+                           w_vals, gw, L.F.view(), (int)ntiles, sp2.tps, part, pstride, (int)nB);
+    else
+        hipLaunchKernelGGL(k_conv_bwd_fused<spt2::NS>, dim3((unsigned)(ps.begin[4] + nB)), dim3(spt2::NTHR), 0, st, ps,
+                           w_vals, gw, L.F.view(), (int)ntiles, sp2.tps, part, pstride, (int)nB);
     SP_CHECK_LAUNCH();
     return spt2::slot_reduce(L.F, part, sp2.nsplit, pstride, dW, st);
 }

@@ -251,12 +251,13 @@ struct LinGeo2 {
     }
     // Accumulators -> Out through LDS: ys[position][token], then each thread
     // writes one row position for a stride of tokens (row segments coalesce).
-    __device__ void store(float *ys, const float (&acc)[spt2::NS][4], const Tok &, int64_t t0, int64_t row0,
+    template <int NSA>
+    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &, int64_t t0, int64_t row0,
                           bool add) const {
         const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
         __syncthreads();
 #pragma unroll
-        for (int s = 0; s < spt2::NS; ++s) {
+        for (int s = 0; s < NSA; ++s) {
             const int pos = spt2::NG * spt2::NW * s + spt2::NG * w + g;
 #pragma unroll
             for (int k = 0; k < 4; ++k) ys[pos * spt2::YS + 4 * gl + k] = acc[s][k];

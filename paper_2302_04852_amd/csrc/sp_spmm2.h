@@ -180,8 +180,11 @@ __device__ inline void slot_vals(float (&v)[PRE], const int2 (&m)[PRE], const fl
 // and independent of their order, since 0 + a + b = 0 + b + a.  spmm2_tile
 // runs one work item in the calling workgroup, staging through xs (LDS,
 // XS_FLOATS floats); k_spmm2 launches the items of one product, a kernel may
-// also pick among several products by block.
-template <class Geo>
+// also pick among several products by block.  NSA < NS processes only the
+// first NSA slots of every wave: for a single panel of at most 32*NSA rows,
+// whose other slots are empty, no metadata is requested for them and their
+// accumulators are not held.
+template <class Geo, int NSA = NS>
 __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const SlotView &tv, int ntiles, int nks,
                            int L, float *xs) {
     const int tid = threadIdx.x, lane = tid & 63;
@@ -195,9 +198,9 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
     typename Geo::Tok tok;
     geo.tile_init(tok, t0);
 
-    float acc[NS][4];
+    float acc[NSA][4];
 #pragma unroll
-    for (int s = 0; s < NS; ++s) acc[s][0] = acc[s][1] = acc[s][2] = acc[s][3] = 0.f;
+    for (int s = 0; s < NSA; ++s) acc[s][0] = acc[s][1] = acc[s][2] = acc[s][3] = 0.f;
 
     const int K = tv.K;
     const int k0 = (int)((int64_t)ks * K / nks), k1 = (int)((int64_t)(ks + 1) * K / nks);
@@ -212,8 +215,8 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
     // are not held through the product loop, and the second workgroup
     // resident on the compute unit covers the load latency.
     SlotHdr hc, hn;
-    int2 mt[NS + 2][PRE];
-    float vv[NS + 1][PRE];
+    int2 mt[NSA + 2][PRE];
+    float vv[NSA + 1][PRE];
     if (k0 < k1) {
         hc.load(tv, p, k0, w);
         slot_meta(mt[0], tv, hc.bs[0], hc.ms[0], lp);
@@ -231,12 +234,12 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
         const bool more = k + 1 < k1;
         if (more) hn.load(tv, p, k + 1, w);
 #pragma unroll
-        for (int s = 0; s < NS; ++s) {
-            if (s + 2 < NS)
+        for (int s = 0; s < NSA; ++s) {
+            if (s + 2 < NSA)
                 slot_meta(mt[s + 2], tv, hc.bs[s + 2], hc.ms[s + 2], lp);
             else if (more)
-                slot_meta(mt[s + 2], tv, hn.bs[s + 2 - NS], hn.ms[s + 2 - NS], lp);
-            if (s + 1 < NS || more) slot_vals(vv[s + 1], mt[s + 1], vals);
+                slot_meta(mt[s + 2], tv, hn.bs[s + 2 - NSA], hn.ms[s + 2 - NSA], lp);
+            if (s + 1 < NSA || more) slot_vals(vv[s + 1], mt[s + 1], vals);
             for (int blk = 0, m = hc.ms[s]; m > 0; ++blk, m -= 16) {
                 int off;
                 float val;
@@ -256,20 +259,20 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
             hc = hn;
 #pragma unroll
             for (int u = 0; u < PRE; ++u) {
-                mt[0][u] = mt[NS][u];
-                mt[1][u] = mt[NS + 1][u];
-                vv[0][u] = vv[NS][u];
+                mt[0][u] = mt[NSA][u];
+                mt[1][u] = mt[NSA + 1][u];
+                vv[0][u] = vv[NSA][u];
             }
         }
     }
     geo.store(xs, acc, tok, t0, (int64_t)p * R, nks > 1);
 }
 
-template <class Geo>
+template <class Geo, int NSA = NS>
 __global__ __launch_bounds__(NTHR) void k_spmm2(Geo geo, const float *__restrict__ vals, SlotView tv, int ntiles,
                                                 int nks) {
     __shared__ __attribute__((aligned(16))) float xs[XS_FLOATS];
-    spmm2_tile(geo, vals, tv, ntiles, nks, sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks), xs);
+    spmm2_tile<Geo, NSA>(geo, vals, tv, ntiles, nks, sp::xcd_remap(blockIdx.x, tv.P * ntiles * nks), xs);
 }
 
 
