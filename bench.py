@@ -53,6 +53,8 @@ HBM_PEAK_GBS = 8000.0
 # FP32 FMA on the vector ALUs, one FMA per lane per clock (packed FP32 is not
 # used): 256 CUs x 4 SIMD x 16 lanes x 2 flop x 2.4 GHz.
 VALU_FP32_PEAK_TFLOPS = 256 * 4 * 16 * 2 * 2.4e9 / 1e12
+# FP32 on the matrix cores (v_mfma_f32_32x32x2_f32), MI355X's published dense peak.
+MFMA_FP32_PEAK_TFLOPS = 157.3
 WORKLOADS = ("ffn", "linear_small", "conv3x3_56", "conv_sweep", "resnet18")
 
 
@@ -63,6 +65,11 @@ def parse():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", choices=WORKLOADS, default="ffn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--variant", choices=("auto", "sparse", "dense"), default="auto",
+                    help="linear workloads: auto = the paper's choice per layer (dense below 80%% sparsity, "
+                         "else the faster of one timed step each); sparse/dense force one variant")
+    ap.add_argument("--sparsity", type=float, default=None,
+                    help="linear workloads: override the layers' sparsity (default: the workload's own)")
     ap.add_argument("--cold-reps", type=int, default=10,
                     help="launches per op for the cold-cache per-op medians (0: skip)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
@@ -329,11 +336,15 @@ def op_row(ms, fl, by):
             "hbm_frac": round(by / ms / 1e6 / HBM_PEAK_GBS, 4), "bound": bound_of(fl, by)}
 
 
-def roofline(kernel, kind, fl, by, ms, traffic=None, extra=None):
+def roofline(kernel, kind, fl, by, ms, traffic=None, extra=None, mfma_flops=None):
     """Roofline record of one kernel from its algorithmic flops/bytes per
-    launch and its mean event-timed launch duration (ms)."""
-    bound = bound_of(fl, by)
-    if bound == "alu":
+    launch and its mean event-timed launch duration (ms).  mfma_flops: the
+    dense matrix-core flops of a dense-variant launch, priced against the
+    fp32 matrix-core peak."""
+    bound = "mfma" if mfma_flops else bound_of(fl, by)
+    if bound == "mfma":
+        achieved, peak, unit = mfma_flops / (ms * 1e-3) / 1e12, MFMA_FP32_PEAK_TFLOPS, "TFLOP/s"
+    elif bound == "alu":
         achieved, peak, unit = fl / (ms * 1e-3) / 1e12, VALU_FP32_PEAK_TFLOPS, "TFLOP/s"
     else:
         achieved, peak, unit = by / (ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"
@@ -367,12 +378,13 @@ def hbm_record(bytes_step, ms_per_step):
 def run_linear(args, sp, torch, which):
     from synth import FFN_PAIR, LINEAR_SMALL, linear_layer, seed_for
 
+    spec = FFN_PAIR if which == "ffn" else LINEAR_SMALL
+    sparsity = spec[0][4] if args.sparsity is None else args.sparsity
     if which == "ffn":
-        layers_np = [linear_layer(seed_for(2, li), o, i, B, s) for li, (_, o, i, B, s) in enumerate(FFN_PAIR)]
-        B = FFN_PAIR[0][3]
+        layers_np = [linear_layer(seed_for(2, li), o, i, B, sparsity) for li, (_, o, i, B, _) in enumerate(spec)]
     else:
-        layers_np = [linear_layer(seed_for(1, 0), o, i, B, s) for (_, o, i, B, s) in LINEAR_SMALL]
-        B = LINEAR_SMALL[0][3]
+        layers_np = [linear_layer(seed_for(1, 0), o, i, B, sparsity) for (_, o, i, B, _) in spec]
+    B = spec[0][3]
     L1 = LinearLayer(sp, torch, layers_np[0], "W1")
     X = torch.from_numpy(layers_np[0]["X"]).cuda()
     Y1 = torch.empty(B, L1.out_f, device="cuda")
@@ -389,64 +401,101 @@ def run_linear(args, sp, torch, which):
     ws_bytes = max(max(sp.sp_linear_bwd_weight_ws(B, L.in_f, L.out_f, L.nnz) for L in layers), 1)
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
 
-    def lin_op(name, L, kind, f):
-        flops = (4.0 if kind == "bwd" else 2.0) * L.nnz * B
-        return (name, f, kind, flops, linear_alg_bytes(kind, B, L.in_f, L.out_f, L.nnz), L)
+    # The paper's end-to-end protocol: a layer below 80% sparsity runs dense;
+    # from 80% on one forward+backward step of each variant is timed and the
+    # faster is kept (sp_linear_select).  Selection runs once, before the
+    # timed region, on the layer's own synthetic inputs.
+    choice = {}
+    for L, d in zip(layers, layers_np):
+        if args.variant != "auto":
+            L.variant = sp.SP_VARIANT_DENSE if args.variant == "dense" else sp.SP_VARIANT_SPARSE
+            choice[L.name] = {"variant": args.variant, "forced": True}
+            if args.variant == "dense":
+                L.Wd = torch.empty(L.out_f, L.in_f, device="cuda")
+            continue
+        xs = torch.from_numpy(d["X"]).cuda()
+        dys = torch.from_numpy(d["dY"]).cuda()
+        sws = torch.empty(max(sp.sp_linear_select_ws(B, L.in_f, L.out_f, L.nnz), 1), dtype=torch.uint8,
+                          device="cuda")
+        v, ms = sp.sp_linear_select(xs, dys, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.vals, L.nnz, L.plan,
+                                    torch.empty(B, L.out_f, device="cuda"), torch.empty(B, L.in_f, device="cuda"),
+                                    L.dW, sws, 3)
+        L.variant = v
+        choice[L.name] = {"variant": "dense" if v == sp.SP_VARIANT_DENSE else "sparse",
+                          "ms_sparse_step": round(ms[0], 4), "ms_dense_step": round(ms[1], 4)}
+        del sws
+        if v == sp.SP_VARIANT_DENSE:
+            L.Wd = torch.empty(L.out_f, L.in_f, device="cuda")
+    dws_bytes = max([sp.sp_linear_dense_bwd_weight_ws(B, L.in_f, L.out_f) for L in layers
+                     if L.variant == sp.SP_VARIANT_DENSE] + [1])
+    dws = torch.empty(dws_bytes, dtype=torch.uint8, device="cuda")
 
-    # The backward of a layer is one sp_linear_bwd call: the input gradient
-    # and the weight gradient in one launch (plus the fixed-order reduction).
+    def fwd_op(name, L, x, y):
+        if L.variant == sp.SP_VARIANT_DENSE:
+            def f():
+                sp.sp_linear_densify(L.out_f, L.in_f, L.row_ptr, L.col_idx, L.vals, L.nnz, L.Wd)
+                sp.sp_linear_dense_fwd(x, B, L.in_f, L.out_f, L.Wd, y)
+            return (name, f, "dense_fwd", 2.0 * L.nnz * B, linear_alg_bytes("fwd", B, L.in_f, L.out_f, L.nnz), L)
+        return (name, lambda: sp.sp_linear_fwd(x, B, L.in_f, L.out_f, L.vals, L.nnz, L.plan, y), "fwd",
+                2.0 * L.nnz * B, linear_alg_bytes("fwd", B, L.in_f, L.out_f, L.nnz), L)
+
+    # The backward of a sparse layer is one sp_linear_bwd call: the input
+    # gradient and the weight gradient in one launch (plus the fixed-order
+    # reduction).
+    def bwd_op(name, L, dy, x, dx):
+        by = linear_alg_bytes("bwd", B, L.in_f, L.out_f, L.nnz)
+        if L.variant == sp.SP_VARIANT_DENSE:
+            def f():
+                sp.sp_linear_dense_bwd_input(dy, B, L.in_f, L.out_f, L.Wd, dx)
+                sp.sp_linear_dense_bwd_weight(dy, x, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.nnz, L.dW, dws)
+            return (name, f, "dense_bwd", 4.0 * L.nnz * B, by, L)
+        return (name, lambda: sp.sp_linear_bwd(dy, x, B, L.in_f, L.out_f, L.vals, L.nnz, L.plan, dx, L.dW, ws),
+                "bwd", 4.0 * L.nnz * B, by, L)
+
     if which == "ffn":
-        ops = [
-            lin_op("W1.fwd", L1, "fwd",
-                   lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
-            lin_op("W2.fwd", L2, "fwd",
-                   lambda: sp.sp_linear_fwd(Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, Y2)),
-            lin_op("W2.bwd", L2, "bwd",
-                   lambda: sp.sp_linear_bwd(dY2, Y1, B, L2.in_f, L2.out_f, L2.vals, L2.nnz, L2.plan, dX2, L2.dW,
-                                            ws)),
-            lin_op("W1.bwd", L1, "bwd",
-                   lambda: sp.sp_linear_bwd(dX2, X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1, L1.dW,
-                                            ws)),
-        ]
+        ops = [fwd_op("W1.fwd", L1, X, Y1), fwd_op("W2.fwd", L2, Y1, Y2),
+               bwd_op("W2.bwd", L2, dY2, Y1, dX2), bwd_op("W1.bwd", L1, dX2, X, dX1)]
     else:
-        ops = [
-            lin_op("fwd", L1, "fwd",
-                   lambda: sp.sp_linear_fwd(X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, Y1)),
-            lin_op("bwd", L1, "bwd",
-                   lambda: sp.sp_linear_bwd(dY1, X, B, L1.in_f, L1.out_f, L1.vals, L1.nnz, L1.plan, dX1, L1.dW,
-                                            ws)),
-        ]
+        ops = [fwd_op("fwd", L1, X, Y1), bwd_op("bwd", L1, dY1, X, dX1)]
     ms_per_step, per_op, ms_instr = time_ops(torch, ops, args.steps, args.warmup)
     flops_step = sum(o[3] for o in ops)
     bytes_step = sum(o[4] for o in ops)
 
-    # Dominant kernel: the SpMM kernel serves the forward passes; the fused
-    # backward kernel (input-gradient SpMM and weight-gradient SDDMM in one
-    # launch, then the split reduction) the backward passes.  Both layers of
-    # the pair have the same nnz and the same work per launch.
-    spmm = [t for o, t in zip(ops, per_op) if o[2] == "fwd"]
-    bwd = [t for o, t in zip(ops, per_op) if o[2] == "bwd"]
-    if sum(bwd) >= sum(spmm):
-        dom, dom_ms, kind = "k_bwd_fused+k_slot_reduce", float(np.mean(bwd)), "bwd"
-    else:
-        dom, dom_ms, kind = "k_spmm2", float(np.mean(spmm)), "fwd"
-    # per launch: the mean over the launches of that kind (the two layers'
-    # backward passes move different dense bytes)
+    # Dominant kernel: the kind of op with the largest share of the step.  The
+    # SpMM kernel serves the sparse forward passes; the fused backward kernel
+    # (input-gradient SpMM and weight-gradient SDDMM in one launch, then the
+    # split reduction) the sparse backward passes; the matrix-core GEMM the
+    # dense ones.  Per launch: the mean over the launches of that kind (the
+    # two layers' backward passes move different dense bytes).
+    kinds = sorted({o[2] for o in ops})
+    share = {k: sum(t for o, t in zip(ops, per_op) if o[2] == k) for k in kinds}
+    kind = max(kinds, key=lambda k: share[k])
+    dom_ms = float(np.mean([t for o, t in zip(ops, per_op) if o[2] == kind]))
+    dom = {"fwd": "k_spmm2", "bwd": "k_bwd_fused+k_slot_reduce", "dense_fwd": "k_gemm (after k_scatter_rows)",
+           "dense_bwd": "k_gemm x2 + k_sample_rows"}[kind]
     fl = float(np.mean([o[3] for o in ops if o[2] == kind]))
     by = float(np.mean([o[4] for o in ops if o[2] == kind]))
-    traffic = measured_traffic(dom) if which == "ffn" else None
+    traffic = measured_traffic(dom) if which == "ffn" and not kind.startswith("dense") else None
     if which == "ffn":
-        config = {"workload": "FFN pair W1 768->3072 + W2 3072->768, 95% unstructured sparse, 8192 tokens, "
+        config = {"workload": "FFN pair W1 768->3072 + W2 3072->768, %g%% unstructured sparse, 8192 tokens, "
+                              % (100 * sparsity) +
                               "fwd+bwd (input and weight gradient) of both layers",
-                  "tokens": B, "sparsity": 0.95, "nnz_per_layer": L1.nnz}
+                  "tokens": B, "sparsity": sparsity, "nnz_per_layer": L1.nnz}
     else:
-        config = {"workload": "linear 256->256, 90% unstructured sparse, 16 tokens, fwd+bwd",
-                  "tokens": B, "sparsity": 0.90, "nnz": L1.nnz}
+        config = {"workload": "linear 256->256, %g%% unstructured sparse, 16 tokens, fwd+bwd" % (100 * sparsity),
+                  "tokens": B, "sparsity": sparsity, "nnz": L1.nnz}
+    if args.variant != "auto":
+        config["variant"] = args.variant
     out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
     out["hbm"] = hbm_record(bytes_step, ms_per_step)
     out["ms_per_step_with_op_events"] = round(ms_instr, 5)
-    out["roofline"] = roofline(dom, kind, fl, by, dom_ms, traffic, {"source_hash": kernel_source_hash()})
+    mf = None
+    if kind.startswith("dense"):
+        mf = float(np.mean([(2.0 if kind == "dense_fwd" else 4.0) * B * o[5].in_f * o[5].out_f
+                            for o in ops if o[2] == kind]))
+    out["roofline"] = roofline(dom, kind, fl, by, dom_ms, traffic, {"source_hash": kernel_source_hash()}, mf)
     out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    out["variant_choice"] = choice
     cold = cold_record(torch, args, ops)
     if cold:
         out["cold"] = cold
@@ -526,6 +575,7 @@ def run_conv(args, sp, torch, which):
                         "alg_GBps": round(v[2] / v[0] / 1e6, 1), "bound": bound_of(v[1], v[2])}
                     for k, v in kinds.items()}
     out["ops"] = {o[0]: op_row(t, o[3], o[4]) for o, t in zip(ops, per_op)}
+    out["variant_choice"] = choice
     cold = cold_record(torch, args, ops)
     if cold:
         out["cold"] = cold

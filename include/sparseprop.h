@@ -11,7 +11,7 @@
  *    never allocates, frees or keeps a pointer after a call returns.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
  *    device operation is enqueued asynchronously on it; no call synchronises
- *    the host.  Callers must keep inputs alive and unmodified until the
+ *    the host, except sp_linear_select (it reads its timings back).  Callers must keep inputs alive and unmodified until the
  *    stream has passed the call.
  *  - Outputs are overwritten, never accumulated: Y and dX include exact zeros
  *    where no stored weight contributes, and dW holds exactly one value per
@@ -178,6 +178,77 @@ sp_status sp_linear_bwd(const float *dY, const float *X, int64_t B, int64_t in_f
                         int64_t out_f, const float *vals, int64_t nnz,
                         const void *plan, float *dX, float *dW, void *workspace,
                         size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Dense variant and the choice between the variants (Sec. 4, end-to-end     */
+/* training experiments: a module below 80% sparsity runs dense; from 80% on */
+/* one batch of forward + backward is timed through both versions and the    */
+/* faster is kept).                                                          */
+/* ------------------------------------------------------------------------ */
+
+#define SP_VARIANT_SPARSE 0
+#define SP_VARIANT_DENSE 1
+
+/* Dense copy of the layer's weight: Wd [out_f][in_f] receives vals at the
+ * stored (row, col_idx) positions and exact zeros everywhere else.  CSR as in
+ * sp_linear_encode_fill.  Re-run whenever vals change. */
+sp_status sp_linear_densify(int64_t out_f, int64_t in_f, const int32_t *row_ptr,
+                            const int32_t *col_idx, const float *vals, int64_t nnz,
+                            float *Wd, void *stream);
+
+/* Dense forward pass on the matrix cores: Y = X Wd^T, X [B][in_f], Wd from
+ * sp_linear_densify, Y out [B][out_f].  Same result as sp_linear_fwd up to
+ * the order of the fp32 additions (pruned positions add exact zeros; a
+ * non-finite X value at a pruned position propagates, which it does not in
+ * the sparse variant). */
+sp_status sp_linear_dense_fwd(const float *X, int64_t B, int64_t in_f, int64_t out_f,
+                              const float *Wd, float *Y, void *stream);
+
+/* Dense input gradient on the matrix cores: dX = dY Wd, dY [B][out_f],
+ * dX out [B][in_f].  Same result as sp_linear_bwd_input up to the order of
+ * the additions. */
+sp_status sp_linear_dense_bwd_input(const float *dY, int64_t B, int64_t in_f,
+                                    int64_t out_f, const float *Wd, float *dX,
+                                    void *stream);
+
+/* Workspace bytes needed by sp_linear_dense_bwd_weight (host). */
+sp_status sp_linear_dense_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f,
+                                        size_t *bytes);
+
+/* Dense weight gradient sampled at the stored entries: the full product
+ * dY^T X is formed on the matrix cores (in token-range splits, into the
+ * workspace) and dW[j] = sum of the splits at (row(j), col_idx[j]), added in
+ * split order (deterministic).  CSR as in sp_linear_encode_fill; dW out [nnz]
+ * in CSR order.  Same result as sp_linear_bwd_weight up to the order of the
+ * additions. */
+sp_status sp_linear_dense_bwd_weight(const float *dY, const float *X, int64_t B,
+                                     int64_t in_f, int64_t out_f,
+                                     const int32_t *row_ptr, const int32_t *col_idx,
+                                     int64_t nnz, float *dW, void *workspace,
+                                     size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by sp_linear_select (host). */
+sp_status sp_linear_select_ws(int64_t B, int64_t in_f, int64_t out_f, int64_t nnz,
+                              size_t *bytes);
+
+/* Choice of variant for one layer.  With more than 20% of the weights stored
+ * (below 80% sparsity) *variant = SP_VARIANT_DENSE and nothing runs.
+ * Otherwise one step of each variant runs untimed, then `reps` steps of each
+ * are timed with HIP events on the stream, and the faster is chosen; B == 0
+ * or nnz == 0 choose SP_VARIANT_SPARSE untimed.  A sparse step is
+ * sp_linear_fwd + sp_linear_bwd; a dense step is sp_linear_densify +
+ * sp_linear_dense_fwd + sp_linear_dense_bwd_input + sp_linear_dense_bwd_weight.
+ * Inputs X, dY, CSR, vals and plan as in those calls; Y, dX, dW are
+ * overwritten with the layer's outputs by the timed steps.  variant: host
+ * out; ms: host out [2], mean milliseconds per step of the sparse and the
+ * dense variant (-1 where not timed).  workspace: sp_linear_select_ws()
+ * bytes.  Unlike every other call, this one waits for the stream (it reads
+ * the timings back on the host). */
+sp_status sp_linear_select(const float *X, const float *dY, int64_t B, int64_t in_f,
+                           int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
+                           const float *vals, int64_t nnz, const void *plan, float *Y,
+                           float *dX, float *dW, void *workspace, size_t ws_bytes,
+                           int reps, int *variant, float *ms, void *stream);
 
 /* Host.  Structural check of a CSR pattern held in HOST memory: returns
  * SP_OK or SP_ERR_INVALID_ARG (row_ptr not monotone, row_ptr[0] != 0,

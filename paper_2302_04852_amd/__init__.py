@@ -26,6 +26,7 @@ if not os.path.exists(LIB_PATH):
 _lib = ctypes.CDLL(LIB_PATH)
 
 SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_HIP, SP_ERR_WORKSPACE = 0, 1, 2, 3, 4
+SP_VARIANT_SPARSE, SP_VARIANT_DENSE = 0, 1
 
 
 class SparsePropError(RuntimeError):
@@ -65,6 +66,14 @@ _SIGS = {
     "sp_linear_bwd_weight": [_P, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _SZ, _P],
     "sp_linear_bwd": [_P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_linear_validate": [_I64, _I64, _P, _P, _I64],
+    "sp_linear_densify": [_I64, _I64, _P, _P, _P, _I64, _P, _P],
+    "sp_linear_dense_fwd": [_P, _I64, _I64, _I64, _P, _P, _P],
+    "sp_linear_dense_bwd_input": [_P, _I64, _I64, _I64, _P, _P, _P],
+    "sp_linear_dense_bwd_weight_ws": [_I64, _I64, _I64, ctypes.POINTER(_SZ)],
+    "sp_linear_dense_bwd_weight": [_P, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _SZ, _P],
+    "sp_linear_select_ws": [_I64, _I64, _I64, _I64, ctypes.POINTER(_SZ)],
+    "sp_linear_select": [_P, _P, _I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _I32,
+                         ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _P],
     "sp_conv_out_hw": [ctypes.POINTER(ConvShape), ctypes.POINTER(_I64), ctypes.POINTER(_I64)],
     "sp_conv_encode_rows": [_I64, _I64, _I32, _I32, _P, _P, _P, _P],
     "sp_conv_encode_fill": [_I64, _I64, _I32, _I32, _P, _P, _P, _P, _P, _P, _P, _P],
@@ -193,6 +202,47 @@ def sp_linear_bwd(dY, X, B, in_f, out_f, vals, nnz, plan, dX, dW, workspace, str
     nbytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _call("sp_linear_bwd", _ptr(dY), _ptr(X), B, in_f, out_f, _ptr(vals), nnz, _ptr(plan), _ptr(dX), _ptr(dW),
           _ptr(workspace), nbytes, _stream(stream))
+
+
+def _nbytes(t):
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def sp_linear_densify(out_f, in_f, row_ptr, col_idx, vals, nnz, Wd, stream=None):
+    _call("sp_linear_densify", out_f, in_f, _ptr(row_ptr), _ptr(col_idx), _ptr(vals), nnz, _ptr(Wd),
+          _stream(stream))
+
+
+def sp_linear_dense_fwd(X, B, in_f, out_f, Wd, Y, stream=None):
+    _call("sp_linear_dense_fwd", _ptr(X), B, in_f, out_f, _ptr(Wd), _ptr(Y), _stream(stream))
+
+
+def sp_linear_dense_bwd_input(dY, B, in_f, out_f, Wd, dX, stream=None):
+    _call("sp_linear_dense_bwd_input", _ptr(dY), B, in_f, out_f, _ptr(Wd), _ptr(dX), _stream(stream))
+
+
+def sp_linear_dense_bwd_weight_ws(B, in_f, out_f):
+    return _ws("sp_linear_dense_bwd_weight_ws", B, in_f, out_f)
+
+
+def sp_linear_dense_bwd_weight(dY, X, B, in_f, out_f, row_ptr, col_idx, nnz, dW, workspace, stream=None):
+    _call("sp_linear_dense_bwd_weight", _ptr(dY), _ptr(X), B, in_f, out_f, _ptr(row_ptr), _ptr(col_idx), nnz,
+          _ptr(dW), _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def sp_linear_select_ws(B, in_f, out_f, nnz):
+    return _ws("sp_linear_select_ws", B, in_f, out_f, nnz)
+
+
+def sp_linear_select(X, dY, B, in_f, out_f, row_ptr, col_idx, vals, nnz, plan, Y, dX, dW, workspace, reps=3,
+                     stream=None):
+    """Returns (variant, [ms_sparse, ms_dense]); waits for the stream."""
+    variant = ctypes.c_int(-1)
+    ms = (ctypes.c_float * 2)()
+    _call("sp_linear_select", _ptr(X), _ptr(dY), B, in_f, out_f, _ptr(row_ptr), _ptr(col_idx), _ptr(vals), nnz,
+          _ptr(plan), _ptr(Y), _ptr(dX), _ptr(dW), _ptr(workspace), _nbytes(workspace), reps,
+          ctypes.byref(variant), ms, _stream(stream))
+    return int(variant.value), [float(ms[0]), float(ms[1])]
 
 
 def sp_linear_validate(in_f, out_f, row_ptr, col_idx, nnz):

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsparseprop.so")
-SOURCES = ["sp_common.hip", "sp_slots.hip", "sp_linear.hip", "sp_conv.hip"]
+SOURCES = ["sp_common.hip", "sp_slots.hip", "sp_linear.hip", "sp_conv.hip", "sp_dense.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
