@@ -11,7 +11,8 @@
  *    never allocates, frees or keeps a pointer after a call returns.
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
  *    device operation is enqueued asynchronously on it; no call synchronises
- *    the host, except sp_linear_select (it reads its timings back).  Callers must keep inputs alive and unmodified until the
+ *    the host, except sp_linear_select and sp_conv_select (they read their
+ *    timings back).  Callers must keep inputs alive and unmodified until the
  *    stream has passed the call.
  *  - Outputs are overwritten, never accumulated: Y and dX include exact zeros
  *    where no stored weight contributes, and dW holds exactly one value per
@@ -347,6 +348,64 @@ sp_status sp_conv_bwd_weight(const float *dY, const float *X, const sp_conv_shap
 sp_status sp_conv_bwd(const float *dY, const float *X, const sp_conv_shape *s,
                       const float *w_vals, int64_t nnz, const void *plan, float *dX,
                       float *dW, void *workspace, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Dense variant of a convolution and the choice between the variants       */
+/* (Sec. 4, end-to-end training experiments; the same rule as for linear    */
+/* layers: dense below 80% sparsity, else the faster of one timed step).    */
+/* ------------------------------------------------------------------------ */
+
+/* Dense copy of the weight: Wd [OC][IC][KH][KW] receives w_vals at the stored
+ * (oc, ic, x, y) positions and exact zeros elsewhere.  Re-run whenever the
+ * values change. */
+sp_status sp_conv_densify(const sp_conv_shape *s, const int32_t *w_oc, const int16_t *w_ic,
+                          const uint8_t *w_x, const uint8_t *w_y, const float *w_vals,
+                          int64_t nnz, float *Wd, void *stream);
+
+/* Dense forward pass: an implicit-im2col GEMM on the matrix cores, Wd
+ * [OC][IC*KH*KW] times the (ic, x, y) x (b, p, q) patches of X gathered on the
+ * fly.  X, Y as in sp_conv_fwd; same result up to the order of the fp32
+ * additions (non-finite X values under pruned taps propagate here). */
+sp_status sp_conv_dense_fwd(const float *X, const sp_conv_shape *s, const float *Wd, float *Y,
+                            void *stream);
+
+/* Workspace bytes needed by sp_conv_dense_bwd_input (host). */
+sp_status sp_conv_dense_bwd_input_ws(const sp_conv_shape *s, size_t *bytes);
+
+/* Dense input gradient: the weight transposed to [IC][OC*KH*KW] in the
+ * workspace, then a GEMM against the dY values each input pixel's taps reach
+ * (zero where the stride skips a tap or it falls outside).  dY, dX as in
+ * sp_conv_bwd_input. */
+sp_status sp_conv_dense_bwd_input(const float *dY, const sp_conv_shape *s, const float *Wd,
+                                  float *dX, void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by sp_conv_dense_bwd_weight (host). */
+sp_status sp_conv_dense_bwd_weight_ws(const sp_conv_shape *s, size_t *bytes);
+
+/* Dense weight gradient sampled at the stored entries: dY [OC][(b,p,q)] times
+ * the im2col patches of X, in output-pixel splits (partials in the
+ * workspace), summed in split order at each stored entry (deterministic).
+ * dW out [nnz] in the format's entry order. */
+sp_status sp_conv_dense_bwd_weight(const float *dY, const float *X, const sp_conv_shape *s,
+                                   const int32_t *w_oc, const int16_t *w_ic,
+                                   const uint8_t *w_x, const uint8_t *w_y, int64_t nnz,
+                                   float *dW, void *workspace, size_t ws_bytes, void *stream);
+
+/* Workspace bytes needed by sp_conv_select (host). */
+sp_status sp_conv_select_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
+
+/* Choice of variant for one conv layer, as sp_linear_select: below 80%
+ * sparsity SP_VARIANT_DENSE untimed; otherwise one step of each variant
+ * untimed, `reps` timed steps of each, the faster chosen (B == 0 or nnz == 0:
+ * SP_VARIANT_SPARSE untimed).  A sparse step is sp_conv_fwd + sp_conv_bwd; a
+ * dense step is sp_conv_densify + sp_conv_dense_fwd + sp_conv_dense_bwd_input
+ * + sp_conv_dense_bwd_weight.  Y, dX, dW receive the layer's outputs.
+ * variant, ms[2]: host out.  Waits for the stream. */
+sp_status sp_conv_select(const float *X, const float *dY, const sp_conv_shape *s,
+                         const int32_t *w_oc, const int16_t *w_ic, const uint8_t *w_x,
+                         const uint8_t *w_y, const float *w_vals, int64_t nnz,
+                         const void *plan, float *Y, float *dX, float *dW, void *workspace,
+                         size_t ws_bytes, int reps, int *variant, float *ms, void *stream);
 
 /* Host.  Structural check of a five-array pattern held in HOST memory. */
 sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW,

@@ -86,6 +86,15 @@ _SIGS = {
     "sp_conv_bwd_weight": [_P, _P, ctypes.POINTER(ConvShape), _I64, _P, _P, _P, _SZ, _P],
     "sp_conv_bwd": [_P, _P, ctypes.POINTER(ConvShape), _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_conv_validate": [_I64, _I64, _I32, _I32, _P, _P, _P, _P, _I64],
+    "sp_conv_densify": [ctypes.POINTER(ConvShape), _P, _P, _P, _P, _P, _I64, _P, _P],
+    "sp_conv_dense_fwd": [_P, ctypes.POINTER(ConvShape), _P, _P, _P],
+    "sp_conv_dense_bwd_input_ws": [ctypes.POINTER(ConvShape), ctypes.POINTER(_SZ)],
+    "sp_conv_dense_bwd_input": [_P, ctypes.POINTER(ConvShape), _P, _P, _P, _SZ, _P],
+    "sp_conv_dense_bwd_weight_ws": [ctypes.POINTER(ConvShape), ctypes.POINTER(_SZ)],
+    "sp_conv_dense_bwd_weight": [_P, _P, ctypes.POINTER(ConvShape), _P, _P, _P, _P, _I64, _P, _P, _SZ, _P],
+    "sp_conv_select_ws": [ctypes.POINTER(ConvShape), _I64, ctypes.POINTER(_SZ)],
+    "sp_conv_select": [_P, _P, ctypes.POINTER(ConvShape), _P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _I32,
+                       ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _P],
 }
 
 EXPORTED = sorted(_SIGS) + ["sp_status_string", "sp_version"]
@@ -311,3 +320,45 @@ def sp_conv_validate(OC, IC, KH, KW, w_oc, w_ic, w_x, w_y, nnz):
     """Host arrays (numpy)."""
     _call("sp_conv_validate", OC, IC, KH, KW, _host_ptr(w_oc), _host_ptr(w_ic), _host_ptr(w_x),
           _host_ptr(w_y), nnz)
+
+
+def sp_conv_densify(shape: ConvShape, w_oc, w_ic, w_x, w_y, w_vals, nnz, Wd, stream=None):
+    _call("sp_conv_densify", ctypes.byref(shape), _ptr(w_oc), _ptr(w_ic), _ptr(w_x), _ptr(w_y), _ptr(w_vals), nnz,
+          _ptr(Wd), _stream(stream))
+
+
+def sp_conv_dense_fwd(X, shape: ConvShape, Wd, Y, stream=None):
+    _call("sp_conv_dense_fwd", _ptr(X), ctypes.byref(shape), _ptr(Wd), _ptr(Y), _stream(stream))
+
+
+def sp_conv_dense_bwd_input_ws(shape: ConvShape):
+    return _ws("sp_conv_dense_bwd_input_ws", ctypes.byref(shape))
+
+
+def sp_conv_dense_bwd_input(dY, shape: ConvShape, Wd, dX, workspace, stream=None):
+    _call("sp_conv_dense_bwd_input", _ptr(dY), ctypes.byref(shape), _ptr(Wd), _ptr(dX), _ptr(workspace),
+          _nbytes(workspace), _stream(stream))
+
+
+def sp_conv_dense_bwd_weight_ws(shape: ConvShape):
+    return _ws("sp_conv_dense_bwd_weight_ws", ctypes.byref(shape))
+
+
+def sp_conv_dense_bwd_weight(dY, X, shape: ConvShape, w_oc, w_ic, w_x, w_y, nnz, dW, workspace, stream=None):
+    _call("sp_conv_dense_bwd_weight", _ptr(dY), _ptr(X), ctypes.byref(shape), _ptr(w_oc), _ptr(w_ic), _ptr(w_x),
+          _ptr(w_y), nnz, _ptr(dW), _ptr(workspace), _nbytes(workspace), _stream(stream))
+
+
+def sp_conv_select_ws(shape: ConvShape, nnz):
+    return _ws("sp_conv_select_ws", ctypes.byref(shape), nnz)
+
+
+def sp_conv_select(X, dY, shape: ConvShape, w_oc, w_ic, w_x, w_y, w_vals, nnz, plan, Y, dX, dW, workspace, reps=3,
+                   stream=None):
+    """Returns (variant, [ms_sparse, ms_dense]); waits for the stream."""
+    variant = ctypes.c_int(-1)
+    ms = (ctypes.c_float * 2)()
+    _call("sp_conv_select", _ptr(X), _ptr(dY), ctypes.byref(shape), _ptr(w_oc), _ptr(w_ic), _ptr(w_x), _ptr(w_y),
+          _ptr(w_vals), nnz, _ptr(plan), _ptr(Y), _ptr(dX), _ptr(dW), _ptr(workspace), _nbytes(workspace), reps,
+          ctypes.byref(variant), ms, _stream(stream))
+    return int(variant.value), [float(ms[0]), float(ms[1])]
