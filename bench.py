@@ -66,8 +66,8 @@ def parse():
     ap.add_argument("--workload", choices=WORKLOADS, default="ffn")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--variant", choices=("auto", "sparse", "dense"), default="auto",
-                    help="linear workloads: auto = the paper's choice per layer (dense below 80%% sparsity, "
-                         "else the faster of one timed step each); sparse/dense force one variant")
+                    help="auto = the paper's choice per layer (dense below 80%% sparsity, else the faster of "
+                         "one timed step each); sparse/dense force one variant for every layer")
     ap.add_argument("--sparsity", type=float, default=None,
                     help="linear workloads: override the layers' sparsity (default: the workload's own)")
     ap.add_argument("--cold-reps", type=int, default=10,
@@ -160,6 +160,14 @@ def bound_of(flops, nbytes):
 
 # --------------------------------------------------------------------- layers
 
+def select_flags(sp, sparsity):
+    """The paper applies its 80% rule to a layer's pruning target; the synthetic
+    masks are Bernoulli draws that land a little above or below it.  Layers
+    pruned to 80% or more are therefore always timed; below that the
+    library's rule (dense, untimed) applies."""
+    return sp.SP_SELECT_ALWAYS_TIME if sparsity >= 0.8 else 0
+
+
 class LinearLayer:
     def __init__(self, sp, torch, d, name):
         self.name = name
@@ -188,6 +196,7 @@ class ConvLayer:
         from synth import conv_layer
         name, B, IC, H, W, OC, KH, KW, s, p, sparsity = spec
         self.name = name
+        self.sparsity = sparsity
         self.dims = (B, IC, H, W, OC, KH, KW)
         self.shape = sp.conv_shape(B, IC, H, W, OC, KH, KW, (s, s), (p, p))
         self.OH, self.OW = sp.sp_conv_out_hw(self.shape)
@@ -219,11 +228,42 @@ class ConvLayer:
                               device=dev)
         self.mask_np, self.W_np = d["mask"], d["W"]
 
+    def select(self, sp, torch, mode):
+        """The paper's per-layer choice (sp_conv_select), or a forced variant."""
+        if mode != "auto":
+            self.variant = sp.SP_VARIANT_DENSE if mode == "dense" else sp.SP_VARIANT_SPARSE
+            self.choice = {"variant": mode, "forced": True}
+        else:
+            ws = torch.empty(max(sp.sp_conv_select_ws(self.shape, self.nnz), 1), dtype=torch.uint8, device="cuda")
+            v, ms = sp.sp_conv_select(self.X, self.dY, self.shape, self.w_oc, self.w_ic, self.w_x, self.w_y,
+                                      self.w_vals, self.nnz, self.plan, self.Y, self.dX, self.dW, ws, 3,
+                                      select_flags(sp, self.sparsity))
+            del ws
+            self.variant = v
+            self.choice = {"variant": "dense" if v == sp.SP_VARIANT_DENSE else "sparse",
+                           "ms_sparse_step": round(ms[0], 4), "ms_dense_step": round(ms[1], 4)}
+        if self.variant == sp.SP_VARIANT_DENSE:
+            B, IC, H, W, OC, KH, KW = self.dims
+            self.Wd = torch.empty(OC, IC, KH, KW, device="cuda")
+            self.dws = torch.empty(max(sp.sp_conv_dense_ws(self.shape), 1), dtype=torch.uint8, device="cuda")
+
     def ops(self, sp):
         B, IC, H, W, OC, KH, KW = self.dims
         fl = 2.0 * self.nnz * B * self.OH * self.OW
         by = conv_alg_bytes(B, IC, H, W, OC, self.OH, self.OW, self.nnz)
         by_b = conv_bwd_alg_bytes(B, IC, H, W, OC, self.OH, self.OW, self.nnz)
+        if self.variant == sp.SP_VARIANT_DENSE:
+            def fwd():
+                sp.sp_conv_densify(self.shape, self.w_oc, self.w_ic, self.w_x, self.w_y, self.w_vals, self.nnz,
+                                   self.Wd)
+                sp.sp_conv_dense_fwd(self.X, self.shape, self.Wd, self.Y, self.dws)
+
+            def bwd():
+                sp.sp_conv_dense_bwd_input(self.dY, self.shape, self.Wd, self.dX, self.dws)
+                sp.sp_conv_dense_bwd_weight(self.dY, self.X, self.shape, self.w_oc, self.w_ic, self.w_x, self.w_y,
+                                            self.nnz, self.dW, self.dws)
+            return [(self.name + ".fwd", fwd, "dense_fwd", fl, by, self),
+                    (self.name + ".bwd", bwd, "dense_bwd", 2 * fl, by_b, self)]
         # the backward is one sp_conv_bwd call: input and weight gradient
         return [
             (self.name + ".fwd", lambda: sp.sp_conv_fwd(self.X, self.shape, self.w_vals, self.nnz, self.plan, self.Y),
@@ -233,6 +273,10 @@ class ConvLayer:
                                     self.ws),
              "bwd", 2 * fl, by_b, self),
         ]
+
+    def dense_flops(self):
+        B, IC, H, W, OC, KH, KW = self.dims
+        return 2.0 * B * self.OH * self.OW * OC * IC * KH * KW
 
 
 # --------------------------------------------------------------------- timing
@@ -419,14 +463,14 @@ def run_linear(args, sp, torch, which):
                           device="cuda")
         v, ms = sp.sp_linear_select(xs, dys, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.vals, L.nnz, L.plan,
                                     torch.empty(B, L.out_f, device="cuda"), torch.empty(B, L.in_f, device="cuda"),
-                                    L.dW, sws, 3)
+                                    L.dW, sws, 3, select_flags(sp, sparsity))
         L.variant = v
         choice[L.name] = {"variant": "dense" if v == sp.SP_VARIANT_DENSE else "sparse",
                           "ms_sparse_step": round(ms[0], 4), "ms_dense_step": round(ms[1], 4)}
         del sws
         if v == sp.SP_VARIANT_DENSE:
             L.Wd = torch.empty(L.out_f, L.in_f, device="cuda")
-    dws_bytes = max([sp.sp_linear_dense_bwd_weight_ws(B, L.in_f, L.out_f) for L in layers
+    dws_bytes = max([sp.sp_linear_dense_ws(B, L.in_f, L.out_f) for L in layers
                      if L.variant == sp.SP_VARIANT_DENSE] + [1])
     dws = torch.empty(dws_bytes, dtype=torch.uint8, device="cuda")
 
@@ -434,7 +478,7 @@ def run_linear(args, sp, torch, which):
         if L.variant == sp.SP_VARIANT_DENSE:
             def f():
                 sp.sp_linear_densify(L.out_f, L.in_f, L.row_ptr, L.col_idx, L.vals, L.nnz, L.Wd)
-                sp.sp_linear_dense_fwd(x, B, L.in_f, L.out_f, L.Wd, y)
+                sp.sp_linear_dense_fwd(x, B, L.in_f, L.out_f, L.Wd, y, dws)
             return (name, f, "dense_fwd", 2.0 * L.nnz * B, linear_alg_bytes("fwd", B, L.in_f, L.out_f, L.nnz), L)
         return (name, lambda: sp.sp_linear_fwd(x, B, L.in_f, L.out_f, L.vals, L.nnz, L.plan, y), "fwd",
                 2.0 * L.nnz * B, linear_alg_bytes("fwd", B, L.in_f, L.out_f, L.nnz), L)
@@ -446,7 +490,7 @@ def run_linear(args, sp, torch, which):
         by = linear_alg_bytes("bwd", B, L.in_f, L.out_f, L.nnz)
         if L.variant == sp.SP_VARIANT_DENSE:
             def f():
-                sp.sp_linear_dense_bwd_input(dy, B, L.in_f, L.out_f, L.Wd, dx)
+                sp.sp_linear_dense_bwd_input(dy, B, L.in_f, L.out_f, L.Wd, dx, dws)
                 sp.sp_linear_dense_bwd_weight(dy, x, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.nnz, L.dW, dws)
             return (name, f, "dense_bwd", 4.0 * L.nnz * B, by, L)
         return (name, lambda: sp.sp_linear_bwd(dy, x, B, L.in_f, L.out_f, L.vals, L.nnz, L.plan, dx, L.dW, ws),
@@ -523,7 +567,9 @@ CONV_DESC = {
                 "fwd, bwd_input, bwd_weight of every layer (BN/ReLU/pooling not included)",
 }
 CONV_KERNEL = {"fwd": "k_spmm2<ConvGeo<0>>",
-               "bwd": "k_conv_bwd_fused+k_slot_reduce (<= 8 input channels: k_fewrows, then the SDDMM)"}
+               "bwd": "k_conv_bwd_fused+k_slot_reduce (<= 8 input channels: k_fewrows, then the SDDMM)",
+               "dense_fwd": "k_gemm<ConvTokens> (after k_conv_scatter)",
+               "dense_bwd": "k_conv_wt + k_gemm<ConvTokens> + k_gemm<PlaneRows, ConvCols> + k_conv_sample"}
 
 
 def run_conv(args, sp, torch, which):
@@ -531,6 +577,12 @@ def run_conv(args, sp, torch, which):
     layers = []
     for spec, seed in conv_specs(which):
         layers.append(ConvLayer(sp, torch, spec, seed))
+    # The paper's end-to-end protocol, per layer, before the timed region:
+    # dense below 80% sparsity, else the faster of one timed step each.
+    choice = {}
+    for L in layers:
+        L.select(sp, torch, args.variant)
+        choice[L.name] = L.choice
     ops = []
     for L in layers:
         ops += L.ops(sp)
@@ -544,11 +596,36 @@ def run_conv(args, sp, torch, which):
         Y = torch.empty(B, o_f, device="cuda")
         dX = torch.empty(B, i_f, device="cuda")
         ws = torch.empty(max(sp.sp_linear_bwd_weight_ws(B, i_f, o_f, fc.nnz), 1), dtype=torch.uint8, device="cuda")
-        for kind, f in (("fwd", lambda: sp.sp_linear_fwd(X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, Y)),
-                        ("bwd", lambda: sp.sp_linear_bwd(dY, X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, dX, fc.dW,
-                                                         ws))):
-            ops.append(("fc." + kind, f, kind, (4.0 if kind == "bwd" else 2.0) * fc.nnz * B,
-                        linear_alg_bytes(kind, B, i_f, o_f, fc.nnz), fc))
+        if args.variant == "auto":
+            sws = torch.empty(max(sp.sp_linear_select_ws(B, i_f, o_f, fc.nnz), 1), dtype=torch.uint8, device="cuda")
+            v, ms = sp.sp_linear_select(X, dY, B, i_f, o_f, fc.row_ptr, fc.col_idx, fc.vals, fc.nnz, fc.plan, Y, dX,
+                                        fc.dW, sws, 3, select_flags(sp, s))
+            del sws
+            choice["fc"] = {"variant": "dense" if v == sp.SP_VARIANT_DENSE else "sparse",
+                            "ms_sparse_step": round(ms[0], 4), "ms_dense_step": round(ms[1], 4)}
+        else:
+            v = sp.SP_VARIANT_DENSE if args.variant == "dense" else sp.SP_VARIANT_SPARSE
+            choice["fc"] = {"variant": args.variant, "forced": True}
+        if v == sp.SP_VARIANT_DENSE:
+            Wd = torch.empty(o_f, i_f, device="cuda")
+            dws = torch.empty(max(sp.sp_linear_dense_ws(B, i_f, o_f), 1), dtype=torch.uint8, device="cuda")
+
+            def fc_fwd():
+                sp.sp_linear_densify(o_f, i_f, fc.row_ptr, fc.col_idx, fc.vals, fc.nnz, Wd)
+                sp.sp_linear_dense_fwd(X, B, i_f, o_f, Wd, Y, dws)
+
+            def fc_bwd():
+                sp.sp_linear_dense_bwd_input(dY, B, i_f, o_f, Wd, dX, dws)
+                sp.sp_linear_dense_bwd_weight(dY, X, B, i_f, o_f, fc.row_ptr, fc.col_idx, fc.nnz, fc.dW, dws)
+            fc_ops = (("dense_fwd", fc_fwd), ("dense_bwd", fc_bwd))
+        else:
+            fc_ops = (("fwd", lambda: sp.sp_linear_fwd(X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, Y)),
+                      ("bwd", lambda: sp.sp_linear_bwd(dY, X, B, i_f, o_f, fc.vals, fc.nnz, fc.plan, dX, fc.dW,
+                                                       ws)))
+        for kind, f in fc_ops:
+            ops.append(("fc." + kind.replace("dense_", ""), f, kind,
+                        (4.0 if kind.endswith("bwd") else 2.0) * fc.nnz * B,
+                        linear_alg_bytes(kind.replace("dense_", ""), B, i_f, o_f, fc.nnz), fc))
     ms_per_step, per_op, ms_instr = time_ops(torch, ops, args.steps, args.warmup)
     flops_step = sum(o[3] for o in ops)
     bytes_step = sum(o[4] for o in ops)
@@ -566,11 +643,17 @@ def run_conv(args, sp, torch, which):
     t, fl, by, n = kinds[kind]
     config = {"workload": CONV_DESC[which], "layers": len(layers) + (1 if fc else 0),
               "nnz_total": int(sum(L.nnz for L in layers) + (fc.nnz if fc else 0))}
+    if args.variant != "auto":
+        config["variant"] = args.variant
     out = base_record(args, flops_step / (ms_per_step * 1e-3) / 1e9, ms_per_step, config)
     out["hbm"] = hbm_record(bytes_step, ms_per_step)
     out["ms_per_step_with_op_events"] = round(ms_instr, 5)
+    mf = None
+    if kind.startswith("dense"):
+        dl = [o[5] for o in ops if o[2] == kind and isinstance(o[5], ConvLayer)]
+        mf = sum(L.dense_flops() * (2 if kind == "dense_bwd" else 1) for L in dl) / len(dl)
     out["roofline"] = roofline(CONV_KERNEL[kind], kind, fl / n, by / n, t / n, None,
-                               {"launches_per_step": n, "note": "per-launch means over the workload's layers"})
+                               {"launches_per_step": n, "note": "per-launch means over the workload's layers"}, mf)
     out["by_op"] = {k: {"ms": round(v[0], 4), "tflops": round(v[1] / v[0] / 1e9, 3),
                         "alg_GBps": round(v[2] / v[0] / 1e6, 1), "bound": bound_of(v[1], v[2])}
                     for k, v in kinds.items()}

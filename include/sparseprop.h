@@ -189,6 +189,8 @@ sp_status sp_linear_bwd(const float *dY, const float *X, int64_t B, int64_t in_f
 
 #define SP_VARIANT_SPARSE 0
 #define SP_VARIANT_DENSE 1
+/* sp_*_select flag: time both variants at every sparsity, also below 80%. */
+#define SP_SELECT_ALWAYS_TIME 1
 
 /* Dense copy of the layer's weight: Wd [out_f][in_f] receives vals at the
  * stored (row, col_idx) positions and exact zeros everywhere else.  CSR as in
@@ -197,31 +199,35 @@ sp_status sp_linear_densify(int64_t out_f, int64_t in_f, const int32_t *row_ptr,
                             const int32_t *col_idx, const float *vals, int64_t nnz,
                             float *Wd, void *stream);
 
+/* Workspace bytes that serve each of the three dense products below (host).
+ * A product whose output tiles are too few to fill the GPU splits its
+ * reduction dimension and sums the split partial products in a fixed order
+ * (deterministic); the workspace holds those partials. */
+sp_status sp_linear_dense_ws(int64_t B, int64_t in_f, int64_t out_f, size_t *bytes);
+
 /* Dense forward pass on the matrix cores: Y = X Wd^T, X [B][in_f], Wd from
  * sp_linear_densify, Y out [B][out_f].  Same result as sp_linear_fwd up to
  * the order of the fp32 additions (pruned positions add exact zeros; a
  * non-finite X value at a pruned position propagates, which it does not in
- * the sparse variant). */
+ * the sparse variant).  workspace: sp_linear_dense_ws() bytes (may be NULL
+ * when that is 0). */
 sp_status sp_linear_dense_fwd(const float *X, int64_t B, int64_t in_f, int64_t out_f,
-                              const float *Wd, float *Y, void *stream);
+                              const float *Wd, float *Y, void *workspace, size_t ws_bytes,
+                              void *stream);
 
 /* Dense input gradient on the matrix cores: dX = dY Wd, dY [B][out_f],
  * dX out [B][in_f].  Same result as sp_linear_bwd_input up to the order of
- * the additions. */
+ * the additions.  workspace: sp_linear_dense_ws() bytes. */
 sp_status sp_linear_dense_bwd_input(const float *dY, int64_t B, int64_t in_f,
                                     int64_t out_f, const float *Wd, float *dX,
-                                    void *stream);
-
-/* Workspace bytes needed by sp_linear_dense_bwd_weight (host). */
-sp_status sp_linear_dense_bwd_weight_ws(int64_t B, int64_t in_f, int64_t out_f,
-                                        size_t *bytes);
+                                    void *workspace, size_t ws_bytes, void *stream);
 
 /* Dense weight gradient sampled at the stored entries: the full product
  * dY^T X is formed on the matrix cores (in token-range splits, into the
  * workspace) and dW[j] = sum of the splits at (row(j), col_idx[j]), added in
  * split order (deterministic).  CSR as in sp_linear_encode_fill; dW out [nnz]
  * in CSR order.  Same result as sp_linear_bwd_weight up to the order of the
- * additions. */
+ * additions.  workspace: sp_linear_dense_ws() bytes. */
 sp_status sp_linear_dense_bwd_weight(const float *dY, const float *X, int64_t B,
                                      int64_t in_f, int64_t out_f,
                                      const int32_t *row_ptr, const int32_t *col_idx,
@@ -233,23 +239,24 @@ sp_status sp_linear_select_ws(int64_t B, int64_t in_f, int64_t out_f, int64_t nn
                               size_t *bytes);
 
 /* Choice of variant for one layer.  With more than 20% of the weights stored
- * (below 80% sparsity) *variant = SP_VARIANT_DENSE and nothing runs.
- * Otherwise one step of each variant runs untimed, then `reps` steps of each
- * are timed with HIP events on the stream, and the faster is chosen; B == 0
- * or nnz == 0 choose SP_VARIANT_SPARSE untimed.  A sparse step is
- * sp_linear_fwd + sp_linear_bwd; a dense step is sp_linear_densify +
- * sp_linear_dense_fwd + sp_linear_dense_bwd_input + sp_linear_dense_bwd_weight.
- * Inputs X, dY, CSR, vals and plan as in those calls; Y, dX, dW are
- * overwritten with the layer's outputs by the timed steps.  variant: host
- * out; ms: host out [2], mean milliseconds per step of the sparse and the
- * dense variant (-1 where not timed).  workspace: sp_linear_select_ws()
- * bytes.  Unlike every other call, this one waits for the stream (it reads
- * the timings back on the host). */
+ * (below 80% sparsity) *variant = SP_VARIANT_DENSE and nothing runs, unless
+ * flags has SP_SELECT_ALWAYS_TIME.  Otherwise one step of each variant runs
+ * untimed, then `reps` steps of each are timed with HIP events on the
+ * stream, and the faster is chosen; B == 0 or nnz == 0 choose
+ * SP_VARIANT_SPARSE untimed.  A sparse step is sp_linear_fwd + sp_linear_bwd;
+ * a dense step is sp_linear_densify + sp_linear_dense_fwd +
+ * sp_linear_dense_bwd_input + sp_linear_dense_bwd_weight.  Inputs X, dY,
+ * CSR, vals and plan as in those calls; Y, dX, dW are overwritten with the
+ * layer's outputs by the timed steps.  variant: host out; ms: host out [2],
+ * mean milliseconds per step of the sparse and the dense variant (-1 where
+ * not timed).  workspace: sp_linear_select_ws() bytes.  flags: 0 or
+ * SP_SELECT_ALWAYS_TIME.  Unlike the compute calls, this one waits for the
+ * stream (it reads the timings back on the host). */
 sp_status sp_linear_select(const float *X, const float *dY, int64_t B, int64_t in_f,
                            int64_t out_f, const int32_t *row_ptr, const int32_t *col_idx,
                            const float *vals, int64_t nnz, const void *plan, float *Y,
                            float *dX, float *dW, void *workspace, size_t ws_bytes,
-                           int reps, int *variant, float *ms, void *stream);
+                           int reps, int flags, int *variant, float *ms, void *stream);
 
 /* Host.  Structural check of a CSR pattern held in HOST memory: returns
  * SP_OK or SP_ERR_INVALID_ARG (row_ptr not monotone, row_ptr[0] != 0,
@@ -362,30 +369,34 @@ sp_status sp_conv_densify(const sp_conv_shape *s, const int32_t *w_oc, const int
                           const uint8_t *w_x, const uint8_t *w_y, const float *w_vals,
                           int64_t nnz, float *Wd, void *stream);
 
+/* Workspace bytes that serve each of the three dense conv products (host):
+ * the transposed weight of the input gradient and the split partial
+ * products (see sp_linear_dense_ws). */
+sp_status sp_conv_dense_ws(const sp_conv_shape *s, size_t *bytes);
+
 /* Dense forward pass: an implicit-im2col GEMM on the matrix cores, Wd
  * [OC][IC*KH*KW] times the (ic, x, y) x (b, p, q) patches of X gathered on the
  * fly.  X, Y as in sp_conv_fwd; same result up to the order of the fp32
- * additions (non-finite X values under pruned taps propagate here). */
+ * additions (non-finite X values under pruned taps propagate here).
+ * workspace: sp_conv_dense_ws() bytes. */
 sp_status sp_conv_dense_fwd(const float *X, const sp_conv_shape *s, const float *Wd, float *Y,
-                            void *stream);
+                            void *workspace, size_t ws_bytes, void *stream);
 
-/* Workspace bytes needed by sp_conv_dense_bwd_input (host). */
-sp_status sp_conv_dense_bwd_input_ws(const sp_conv_shape *s, size_t *bytes);
-
-/* Dense input gradient: the weight transposed to [IC][OC*KH*KW] in the
- * workspace, then a GEMM against the dY values each input pixel's taps reach
- * (zero where the stride skips a tap or it falls outside).  dY, dX as in
- * sp_conv_bwd_input. */
+/* Dense input gradient, one GEMM per phase class (sh * sw classes; one at
+ * stride 1): the input pixels with (y + pad_h) % sh == ry and
+ * (x + pad_w) % sw == rx are reached only by the taps x = ry + sh*a,
+ * y = rx + sw*b, so each class is a stride-1 transposed convolution over
+ * those taps (the class's weight, input channels as rows, is copied into the
+ * workspace).  dY, dX as in sp_conv_bwd_input.  workspace: sp_conv_dense_ws()
+ * bytes. */
 sp_status sp_conv_dense_bwd_input(const float *dY, const sp_conv_shape *s, const float *Wd,
                                   float *dX, void *workspace, size_t ws_bytes, void *stream);
-
-/* Workspace bytes needed by sp_conv_dense_bwd_weight (host). */
-sp_status sp_conv_dense_bwd_weight_ws(const sp_conv_shape *s, size_t *bytes);
 
 /* Dense weight gradient sampled at the stored entries: dY [OC][(b,p,q)] times
  * the im2col patches of X, in output-pixel splits (partials in the
  * workspace), summed in split order at each stored entry (deterministic).
- * dW out [nnz] in the format's entry order. */
+ * dW out [nnz] in the format's entry order.  workspace: sp_conv_dense_ws()
+ * bytes. */
 sp_status sp_conv_dense_bwd_weight(const float *dY, const float *X, const sp_conv_shape *s,
                                    const int32_t *w_oc, const int16_t *w_ic,
                                    const uint8_t *w_x, const uint8_t *w_y, int64_t nnz,
@@ -395,17 +406,21 @@ sp_status sp_conv_dense_bwd_weight(const float *dY, const float *X, const sp_con
 sp_status sp_conv_select_ws(const sp_conv_shape *s, int64_t nnz, size_t *bytes);
 
 /* Choice of variant for one conv layer, as sp_linear_select: below 80%
- * sparsity SP_VARIANT_DENSE untimed; otherwise one step of each variant
- * untimed, `reps` timed steps of each, the faster chosen (B == 0 or nnz == 0:
- * SP_VARIANT_SPARSE untimed).  A sparse step is sp_conv_fwd + sp_conv_bwd; a
- * dense step is sp_conv_densify + sp_conv_dense_fwd + sp_conv_dense_bwd_input
- * + sp_conv_dense_bwd_weight.  Y, dX, dW receive the layer's outputs.
- * variant, ms[2]: host out.  Waits for the stream. */
+ * sparsity SP_VARIANT_DENSE untimed (unless flags has SP_SELECT_ALWAYS_TIME,
+ * or the layer has fewer than 32 input channels: the dense input gradient
+ * fills its 64-row tiles with IC rows, so such layers are always timed);
+ * otherwise one step of each variant untimed, `reps` timed steps of each, the
+ * faster chosen (B == 0 or nnz == 0: SP_VARIANT_SPARSE untimed).  A sparse
+ * step is sp_conv_fwd + sp_conv_bwd; a dense step is sp_conv_densify +
+ * sp_conv_dense_fwd + sp_conv_dense_bwd_input + sp_conv_dense_bwd_weight.
+ * Y, dX, dW receive the layer's outputs.  variant, ms[2]: host out.  Waits
+ * for the stream. */
 sp_status sp_conv_select(const float *X, const float *dY, const sp_conv_shape *s,
                          const int32_t *w_oc, const int16_t *w_ic, const uint8_t *w_x,
                          const uint8_t *w_y, const float *w_vals, int64_t nnz,
                          const void *plan, float *Y, float *dX, float *dW, void *workspace,
-                         size_t ws_bytes, int reps, int *variant, float *ms, void *stream);
+                         size_t ws_bytes, int reps, int flags, int *variant, float *ms,
+                         void *stream);
 
 /* Host.  Structural check of a five-array pattern held in HOST memory. */
 sp_status sp_conv_validate(int64_t OC, int64_t IC, int32_t KH, int32_t KW,

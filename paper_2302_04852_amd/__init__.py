@@ -27,6 +27,7 @@ _lib = ctypes.CDLL(LIB_PATH)
 
 SP_OK, SP_ERR_INVALID_ARG, SP_ERR_UNSUPPORTED, SP_ERR_HIP, SP_ERR_WORKSPACE = 0, 1, 2, 3, 4
 SP_VARIANT_SPARSE, SP_VARIANT_DENSE = 0, 1
+SP_SELECT_ALWAYS_TIME = 1
 
 
 class SparsePropError(RuntimeError):
@@ -67,12 +68,12 @@ _SIGS = {
     "sp_linear_bwd": [_P, _P, _I64, _I64, _I64, _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_linear_validate": [_I64, _I64, _P, _P, _I64],
     "sp_linear_densify": [_I64, _I64, _P, _P, _P, _I64, _P, _P],
-    "sp_linear_dense_fwd": [_P, _I64, _I64, _I64, _P, _P, _P],
-    "sp_linear_dense_bwd_input": [_P, _I64, _I64, _I64, _P, _P, _P],
-    "sp_linear_dense_bwd_weight_ws": [_I64, _I64, _I64, ctypes.POINTER(_SZ)],
+    "sp_linear_dense_ws": [_I64, _I64, _I64, ctypes.POINTER(_SZ)],
+    "sp_linear_dense_fwd": [_P, _I64, _I64, _I64, _P, _P, _P, _SZ, _P],
+    "sp_linear_dense_bwd_input": [_P, _I64, _I64, _I64, _P, _P, _P, _SZ, _P],
     "sp_linear_dense_bwd_weight": [_P, _P, _I64, _I64, _I64, _P, _P, _I64, _P, _P, _SZ, _P],
     "sp_linear_select_ws": [_I64, _I64, _I64, _I64, ctypes.POINTER(_SZ)],
-    "sp_linear_select": [_P, _P, _I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _I32,
+    "sp_linear_select": [_P, _P, _I64, _I64, _I64, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _I32, _I32,
                          ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _P],
     "sp_conv_out_hw": [ctypes.POINTER(ConvShape), ctypes.POINTER(_I64), ctypes.POINTER(_I64)],
     "sp_conv_encode_rows": [_I64, _I64, _I32, _I32, _P, _P, _P, _P],
@@ -87,14 +88,13 @@ _SIGS = {
     "sp_conv_bwd": [_P, _P, ctypes.POINTER(ConvShape), _P, _I64, _P, _P, _P, _P, _SZ, _P],
     "sp_conv_validate": [_I64, _I64, _I32, _I32, _P, _P, _P, _P, _I64],
     "sp_conv_densify": [ctypes.POINTER(ConvShape), _P, _P, _P, _P, _P, _I64, _P, _P],
-    "sp_conv_dense_fwd": [_P, ctypes.POINTER(ConvShape), _P, _P, _P],
-    "sp_conv_dense_bwd_input_ws": [ctypes.POINTER(ConvShape), ctypes.POINTER(_SZ)],
+    "sp_conv_dense_ws": [ctypes.POINTER(ConvShape), ctypes.POINTER(_SZ)],
+    "sp_conv_dense_fwd": [_P, ctypes.POINTER(ConvShape), _P, _P, _P, _SZ, _P],
     "sp_conv_dense_bwd_input": [_P, ctypes.POINTER(ConvShape), _P, _P, _P, _SZ, _P],
-    "sp_conv_dense_bwd_weight_ws": [ctypes.POINTER(ConvShape), ctypes.POINTER(_SZ)],
     "sp_conv_dense_bwd_weight": [_P, _P, ctypes.POINTER(ConvShape), _P, _P, _P, _P, _I64, _P, _P, _SZ, _P],
     "sp_conv_select_ws": [ctypes.POINTER(ConvShape), _I64, ctypes.POINTER(_SZ)],
     "sp_conv_select": [_P, _P, ctypes.POINTER(ConvShape), _P, _P, _P, _P, _P, _I64, _P, _P, _P, _P, _P, _SZ, _I32,
-                       ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _P],
+                       _I32, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_float), _P],
 }
 
 EXPORTED = sorted(_SIGS) + ["sp_status_string", "sp_version"]
@@ -222,16 +222,18 @@ def sp_linear_densify(out_f, in_f, row_ptr, col_idx, vals, nnz, Wd, stream=None)
           _stream(stream))
 
 
-def sp_linear_dense_fwd(X, B, in_f, out_f, Wd, Y, stream=None):
-    _call("sp_linear_dense_fwd", _ptr(X), B, in_f, out_f, _ptr(Wd), _ptr(Y), _stream(stream))
+def sp_linear_dense_ws(B, in_f, out_f):
+    return _ws("sp_linear_dense_ws", B, in_f, out_f)
 
 
-def sp_linear_dense_bwd_input(dY, B, in_f, out_f, Wd, dX, stream=None):
-    _call("sp_linear_dense_bwd_input", _ptr(dY), B, in_f, out_f, _ptr(Wd), _ptr(dX), _stream(stream))
+def sp_linear_dense_fwd(X, B, in_f, out_f, Wd, Y, workspace, stream=None):
+    _call("sp_linear_dense_fwd", _ptr(X), B, in_f, out_f, _ptr(Wd), _ptr(Y), _ptr(workspace), _nbytes(workspace),
+          _stream(stream))
 
 
-def sp_linear_dense_bwd_weight_ws(B, in_f, out_f):
-    return _ws("sp_linear_dense_bwd_weight_ws", B, in_f, out_f)
+def sp_linear_dense_bwd_input(dY, B, in_f, out_f, Wd, dX, workspace, stream=None):
+    _call("sp_linear_dense_bwd_input", _ptr(dY), B, in_f, out_f, _ptr(Wd), _ptr(dX), _ptr(workspace),
+          _nbytes(workspace), _stream(stream))
 
 
 def sp_linear_dense_bwd_weight(dY, X, B, in_f, out_f, row_ptr, col_idx, nnz, dW, workspace, stream=None):
@@ -244,12 +246,12 @@ def sp_linear_select_ws(B, in_f, out_f, nnz):
 
 
 def sp_linear_select(X, dY, B, in_f, out_f, row_ptr, col_idx, vals, nnz, plan, Y, dX, dW, workspace, reps=3,
-                     stream=None):
+                     flags=0, stream=None):
     """Returns (variant, [ms_sparse, ms_dense]); waits for the stream."""
     variant = ctypes.c_int(-1)
     ms = (ctypes.c_float * 2)()
     _call("sp_linear_select", _ptr(X), _ptr(dY), B, in_f, out_f, _ptr(row_ptr), _ptr(col_idx), _ptr(vals), nnz,
-          _ptr(plan), _ptr(Y), _ptr(dX), _ptr(dW), _ptr(workspace), _nbytes(workspace), reps,
+          _ptr(plan), _ptr(Y), _ptr(dX), _ptr(dW), _ptr(workspace), _nbytes(workspace), reps, flags,
           ctypes.byref(variant), ms, _stream(stream))
     return int(variant.value), [float(ms[0]), float(ms[1])]
 
@@ -327,21 +329,18 @@ def sp_conv_densify(shape: ConvShape, w_oc, w_ic, w_x, w_y, w_vals, nnz, Wd, str
           _ptr(Wd), _stream(stream))
 
 
-def sp_conv_dense_fwd(X, shape: ConvShape, Wd, Y, stream=None):
-    _call("sp_conv_dense_fwd", _ptr(X), ctypes.byref(shape), _ptr(Wd), _ptr(Y), _stream(stream))
+def sp_conv_dense_ws(shape: ConvShape):
+    return _ws("sp_conv_dense_ws", ctypes.byref(shape))
 
 
-def sp_conv_dense_bwd_input_ws(shape: ConvShape):
-    return _ws("sp_conv_dense_bwd_input_ws", ctypes.byref(shape))
+def sp_conv_dense_fwd(X, shape: ConvShape, Wd, Y, workspace, stream=None):
+    _call("sp_conv_dense_fwd", _ptr(X), ctypes.byref(shape), _ptr(Wd), _ptr(Y), _ptr(workspace), _nbytes(workspace),
+          _stream(stream))
 
 
 def sp_conv_dense_bwd_input(dY, shape: ConvShape, Wd, dX, workspace, stream=None):
     _call("sp_conv_dense_bwd_input", _ptr(dY), ctypes.byref(shape), _ptr(Wd), _ptr(dX), _ptr(workspace),
           _nbytes(workspace), _stream(stream))
-
-
-def sp_conv_dense_bwd_weight_ws(shape: ConvShape):
-    return _ws("sp_conv_dense_bwd_weight_ws", ctypes.byref(shape))
 
 
 def sp_conv_dense_bwd_weight(dY, X, shape: ConvShape, w_oc, w_ic, w_x, w_y, nnz, dW, workspace, stream=None):
@@ -354,11 +353,11 @@ def sp_conv_select_ws(shape: ConvShape, nnz):
 
 
 def sp_conv_select(X, dY, shape: ConvShape, w_oc, w_ic, w_x, w_y, w_vals, nnz, plan, Y, dX, dW, workspace, reps=3,
-                   stream=None):
+                   flags=0, stream=None):
     """Returns (variant, [ms_sparse, ms_dense]); waits for the stream."""
     variant = ctypes.c_int(-1)
     ms = (ctypes.c_float * 2)()
     _call("sp_conv_select", _ptr(X), _ptr(dY), ctypes.byref(shape), _ptr(w_oc), _ptr(w_ic), _ptr(w_x), _ptr(w_y),
           _ptr(w_vals), nnz, _ptr(plan), _ptr(Y), _ptr(dX), _ptr(dW), _ptr(workspace), _nbytes(workspace), reps,
-          ctypes.byref(variant), ms, _stream(stream))
+          flags, ctypes.byref(variant), ms, _stream(stream))
     return int(variant.value), [float(ms[0]), float(ms[1])]

@@ -38,12 +38,11 @@ def _dense_all(sp, L, Xd, dYd):
     B = Xd.shape[0]
     Wd = torch.full((L.out_f, L.in_f), float("nan"), device="cuda")
     sp.sp_linear_densify(L.out_f, L.in_f, L.row_ptr, L.col_idx, L.vals, L.nnz, Wd)
+    ws = torch.empty(max(sp.sp_linear_dense_ws(B, L.in_f, L.out_f), 1), dtype=torch.uint8, device="cuda")
     Y = torch.full((B, L.out_f), float("nan"), device="cuda")
-    sp.sp_linear_dense_fwd(Xd, B, L.in_f, L.out_f, Wd, Y)
+    sp.sp_linear_dense_fwd(Xd, B, L.in_f, L.out_f, Wd, Y, ws)
     dX = torch.full((B, L.in_f), float("nan"), device="cuda")
-    sp.sp_linear_dense_bwd_input(dYd, B, L.in_f, L.out_f, Wd, dX)
-    ws = torch.empty(max(sp.sp_linear_dense_bwd_weight_ws(B, L.in_f, L.out_f), 1), dtype=torch.uint8,
-                     device="cuda")
+    sp.sp_linear_dense_bwd_input(dYd, B, L.in_f, L.out_f, Wd, dX, ws)
     dW = torch.full((max(L.nnz, 1),), float("nan"), device="cuda")
     sp.sp_linear_dense_bwd_weight(dYd, Xd, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.nnz, dW, ws)
     return Wd, Y, dX, dW[:L.nnz]
@@ -92,6 +91,8 @@ def test_dense_small_layer_seed0(sp, orc):
     (70, 130, 513, 0.05),
     (384, 256, 1000, 0.5),    # half dense: the regime the dense variant is for
     (256, 130, 4099, 0.3),    # odd k for the weight gradient's token splits
+    (1024, 2048, 16, 0.3),    # few output tiles: forward and input gradient split k and reduce
+    (3000, 70, 40, 0.5),      # in_f not a multiple of 4, split input gradient
 ])
 def test_dense_ragged_shapes(sp, orc, out_f, in_f, B, density):
     mask, W, X, dY = _layer(out_f * 7 + in_f * 3 + B, out_f, in_f, B, density)
@@ -141,7 +142,7 @@ def test_dense_empty_and_degenerate(sp, orc):
     Y = torch.empty(0, 64, device="cuda")
     Wd = torch.empty(64, 48, device="cuda")
     sp.sp_linear_densify(64, 48, L.row_ptr, L.col_idx, L.vals, L.nnz, Wd)
-    sp.sp_linear_dense_fwd(e, 0, 48, 64, Wd, Y)
+    sp.sp_linear_dense_fwd(e, 0, 48, 64, Wd, Y, None)
     torch.cuda.synchronize()
     assert torch.all(dW == 0)
 
@@ -169,14 +170,21 @@ def test_dense_error_paths(sp, orc):
         sp.sp_linear_dense_bwd_weight(dY, X, 8, 16, 32, L.row_ptr, L.col_idx, L.nnz, dW, small)
     assert e.value.status == sp.SP_ERR_WORKSPACE
     with pytest.raises(sp.SparsePropError) as e:
-        sp.sp_linear_dense_fwd(X, 8, 16, 32, None, torch.empty(8, 32, device="cuda"))
+        sp.sp_linear_dense_fwd(X, 8, 16, 32, None, torch.empty(8, 32, device="cuda"), None)
     assert e.value.status == sp.SP_ERR_INVALID_ARG
+    # a shape whose forward splits k needs the workspace
+    assert sp.sp_linear_dense_ws(16, 2048, 1024) > 0
+    Wd = torch.zeros(1024, 2048, device="cuda")
+    with pytest.raises(sp.SparsePropError) as e:
+        sp.sp_linear_dense_fwd(torch.zeros(16, 2048, device="cuda"), 16, 2048, 1024, Wd,
+                               torch.empty(16, 1024, device="cuda"), None)
+    assert e.value.status == sp.SP_ERR_WORKSPACE
     with pytest.raises(sp.SparsePropError) as e:
         sp.sp_linear_densify(32, 16, L.row_ptr, L.col_idx, L.vals, 16 * 32 + 1, torch.empty(32, 16, device="cuda"))
     assert e.value.status == sp.SP_ERR_INVALID_ARG
 
 
-def _select(sp, L, Xd, dYd, reps=2):
+def _select(sp, L, Xd, dYd, reps=2, flags=0):
     import torch
     B = Xd.shape[0]
     ws = torch.empty(max(sp.sp_linear_select_ws(B, L.in_f, L.out_f, L.nnz), 1), dtype=torch.uint8, device="cuda")
@@ -184,7 +192,7 @@ def _select(sp, L, Xd, dYd, reps=2):
     dX = torch.full((B, L.in_f), float("nan"), device="cuda")
     dW = torch.full((max(L.nnz, 1),), float("nan"), device="cuda")
     v, ms = sp.sp_linear_select(Xd, dYd, B, L.in_f, L.out_f, L.row_ptr, L.col_idx, L.vals, L.nnz, L.plan, Y, dX,
-                                dW, ws, reps)
+                                dW, ws, reps, flags)
     return v, ms, Y, dX, dW[:L.nnz]
 
 
@@ -195,6 +203,13 @@ def test_select_below_80_percent_is_dense_untimed(sp, orc):
     v, ms, Y, _, _ = _select(sp, L, torch.from_numpy(X).cuda(), torch.from_numpy(dY).cuda())
     assert v == sp.SP_VARIANT_DENSE and ms == [-1.0, -1.0]
     assert bool(torch.isnan(Y).all()), "nothing runs below 80% sparsity"
+    # asked to time, it times both below 80% too, and the outputs are the layer's
+    v, ms, Y, dX, dW = _select(sp, L, torch.from_numpy(X).cuda(), torch.from_numpy(dY).cuda(),
+                               flags=sp.SP_SELECT_ALWAYS_TIME)
+    assert ms[0] > 0 and ms[1] > 0 and v == (sp.SP_VARIANT_DENSE if ms[1] < ms[0] else sp.SP_VARIANT_SPARSE)
+    torch.cuda.synchronize()
+    Yr, Ya = orc.linear_fwd(X, L.o_rp, L.o_ci, L.o_v, 256)
+    assert_parity(Y.cpu().numpy(), Yr, Ya, "always-time select fwd")
 
 
 @pytest.mark.parametrize("out_f,in_f,B,density", [

@@ -38,14 +38,13 @@ def _dense_all(sp, L, Xd, dYd):
     B, IC, H, Wd_, OC, KH, KW = L.dims[:7]
     Wd = torch.full((OC, IC, KH, KW), float("nan"), device="cuda")
     sp.sp_conv_densify(L.shape, L.w_oc, L.w_ic, L.w_x, L.w_y, L.w_vals, L.nnz, Wd)
+    ws = torch.empty(sp.sp_conv_dense_ws(L.shape), dtype=torch.uint8, device="cuda")
     Y = torch.full((B, OC, L.OH, L.OW), float("nan"), device="cuda")
-    sp.sp_conv_dense_fwd(Xd, L.shape, Wd, Y)
+    sp.sp_conv_dense_fwd(Xd, L.shape, Wd, Y, ws)
     dX = torch.full((B, IC, H, Wd_), float("nan"), device="cuda")
-    wsi = torch.empty(sp.sp_conv_dense_bwd_input_ws(L.shape), dtype=torch.uint8, device="cuda")
-    sp.sp_conv_dense_bwd_input(dYd, L.shape, Wd, dX, wsi)
-    wsw = torch.empty(sp.sp_conv_dense_bwd_weight_ws(L.shape), dtype=torch.uint8, device="cuda")
+    sp.sp_conv_dense_bwd_input(dYd, L.shape, Wd, dX, ws)
     dW = torch.full((max(L.nnz, 1),), float("nan"), device="cuda")
-    sp.sp_conv_dense_bwd_weight(dYd, Xd, L.shape, L.w_oc, L.w_ic, L.w_x, L.w_y, L.nnz, dW, wsw)
+    sp.sp_conv_dense_bwd_weight(dYd, Xd, L.shape, L.w_oc, L.w_ic, L.w_x, L.w_y, L.nnz, dW, ws)
     return Wd, Y, dX, dW[:L.nnz]
 
 
@@ -97,6 +96,8 @@ def test_dense_conv_many_tiles_ragged(sp, orc):
     (32, 256, 14, 14, 256, 3, 3, (1, 1), (1, 1), 0.8, [0, 17, 31]),   # sweep 256@14 at 80%
     (64, 128, 28, 28, 256, 3, 3, (2, 2), (1, 1), 0.5, [0, 29, 63]),   # ResNet-18 layer3.0.conv1 shape, 50%
     (64, 3, 224, 224, 64, 7, 7, (2, 2), (3, 3), 0.5, [0, 63]),        # the stem at 50%
+    (64, 512, 7, 7, 512, 3, 3, (1, 1), (1, 1), 0.5, [0, 63]),         # 7x7 planes: split k, reduce to planes
+    (32, 256, 14, 14, 1024, 1, 1, (1, 1), (0, 0), 0.8, [0, 31]),      # the sweep's 1x1 at 80%
 ])
 def test_dense_conv_full_size(sp, orc, spec):
     B, IC, H, Wd, OC, KH, KW, stride, pad, s, imgs = spec
@@ -121,7 +122,7 @@ def test_dense_conv_empty_and_degenerate(sp, orc):
     sp.sp_conv_dense_bwd_weight(None, None, s0, L.w_oc, L.w_ic, L.w_x, L.w_y, L.nnz, dW, None)
     Wd = torch.empty(7, 5, 3, 3, device="cuda")
     sp.sp_conv_densify(s0, L.w_oc, L.w_ic, L.w_x, L.w_y, L.w_vals, L.nnz, Wd)
-    sp.sp_conv_dense_fwd(None, s0, Wd, None)
+    sp.sp_conv_dense_fwd(None, s0, Wd, None, None)
     torch.cuda.synchronize()
     assert torch.all(dW == 0)
 
@@ -154,7 +155,7 @@ def test_dense_conv_error_paths(sp, orc):
         sp.sp_conv_dense_bwd_weight(dY, X, L.shape, L.w_oc, L.w_ic, L.w_x, L.w_y, L.nnz, dW, small)
     assert e.value.status == sp.SP_ERR_WORKSPACE
     with pytest.raises(sp.SparsePropError) as e:
-        sp.sp_conv_dense_fwd(X, L.shape, None, torch.empty(2, 5, 6, 6, device="cuda"))
+        sp.sp_conv_dense_fwd(X, L.shape, None, torch.empty(2, 5, 6, 6, device="cuda"), None)
     assert e.value.status == sp.SP_ERR_INVALID_ARG
 
 
@@ -173,6 +174,11 @@ def _select(sp, L, Xd, dYd, reps=2):
 def test_conv_select_below_80_percent_is_dense_untimed(sp, orc):
     import torch
     d, dims = _layer(orc, 9600, 2, 16, 10, 10, 24, 3, 3, (1, 1), (1, 1), 0.5)
+    L = GpuConv(sp, orc, d["mask"], d["W"], 2, 10, 10, (1, 1), (1, 1))
+    v, ms, Y, _, _ = _select(sp, L, torch.from_numpy(d["X"]).cuda(), torch.from_numpy(d["dY"]).cuda())
+    assert v == sp.SP_VARIANT_SPARSE or v == sp.SP_VARIANT_DENSE
+    assert ms[0] > 0 and ms[1] > 0, "fewer than 32 input channels: timed at every sparsity"
+    d, dims = _layer(orc, 9601, 2, 40, 10, 10, 24, 3, 3, (1, 1), (1, 1), 0.5)
     L = GpuConv(sp, orc, d["mask"], d["W"], 2, 10, 10, (1, 1), (1, 1))
     v, ms, Y, _, _ = _select(sp, L, torch.from_numpy(d["X"]).cuda(), torch.from_numpy(d["dY"]).cuda())
     assert v == sp.SP_VARIANT_DENSE and ms == [-1.0, -1.0]
