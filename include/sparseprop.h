@@ -17,8 +17,10 @@
  *  - Outputs are overwritten, never accumulated: Y and dX include exact zeros
  *    where no stored weight contributes, and dW holds exactly one value per
  *    stored weight.  Inputs are never modified.
- *  - Values are fp32 and the arithmetic is fp32 fused multiply-add; results
- *    match the exact sum to within ~1e-6 of the sum of absolute terms.
+ *  - Values are fp32 and the arithmetic is fp32: fused multiply-add on the
+ *    vector ALUs in the sparse variant, fp32 matrix-core instructions in the
+ *    dense variant (sp_*_dense_*); results match the exact sum to within ~1e-6
+ *    of the sum of absolute terms.
  *    Integer/structure outputs are exact and deterministic.  All ops are
  *    deterministic: the same inputs give bitwise identical outputs.
  *  - Errors: cheap argument checks run on the host before anything is
