@@ -390,7 +390,7 @@ struct ConvGeo {
     // tid writes token tid & 63 of rows (tid >> 6) + 8j: runs of consecutive
     // pixels of one channel.
     template <int NSA>
-    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &tk, int64_t, int64_t row0,
+    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &tk, int64_t, int64_t row0, int rp,
                           bool add) const {
         const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
         __syncthreads();
@@ -402,7 +402,7 @@ struct ConvGeo {
         }
         __syncthreads();
         if (tk.obase < 0) return;
-        const int nr = (int)min<int64_t>(spt2::R, orows - row0);
+        const int nr = (int)min<int64_t>(rp, orows - row0);
         for (int r = w; r < nr; r += spt2::NW) {
             float *o = Out + tk.obase + (row0 + r) * onpix;
             const float v = ys[r * spt2::YS + lane];
@@ -508,15 +508,15 @@ ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
     L.t_perm = c.take<int32_t>(nnz);
     L.colA = c.take<int32_t>(nnz);
     L.colB = c.take<int32_t>(nnz);
-    spt2::slot_layout(c, L.F, d.OC, d.IC * d.KK, nnz);
-    spt2::slot_layout(c, L.G, d.IC, d.OC * d.KK, nnz);
+    spt2::slot_layout(c, L.F, d.OC, d.IC * d.KK, nnz, spt2::panel_slots(d.OC));
+    spt2::slot_layout(c, L.G, d.IC, d.OC * d.KK, nnz, spt2::panel_slots(d.IC));
     for (int k = 0; k < 4; ++k) {
         ClassPart &cp = L.cls[k];
         cp.tc = tap_class(k, d.KH, d.KW);
         cp.ptr = c.take<int32_t>(d.IC + 1);
         cp.col = c.take<int32_t>(nnz);
         cp.src = c.take<int32_t>(nnz);
-        spt2::slot_layout(c, cp.T, d.IC, d.OC * cp.tc.ncx * cp.tc.ncy, nnz);
+        spt2::slot_layout(c, cp.T, d.IC, d.OC * cp.tc.ncx * cp.tc.ncy, nnz, spt2::panel_slots(d.IC));
     }
     L.cnt = c.take<int32_t>(std::max(d.OC * L.F.K, d.IC * L.G.K));
     L.bytes = c.off;
@@ -687,8 +687,9 @@ int spmm_splits(const spt2::SlotTiling &t, int64_t ntok) {
 // Slots a SpMM over tiling t has to process: a single panel of at most 64
 // or 128 rows fills only the first 2 or 4 slots of every wave.
 int active_slots(const spt2::SlotTiling &t) {
-    if (t.P != 1) return spt2::NS;
-    return t.rows <= 2 * spt2::NG * spt2::NW ? 2 : t.rows <= 4 * spt2::NG * spt2::NW ? 4 : spt2::NS;
+    if (t.P == 1 && t.rows <= 2 * spt2::NG * spt2::NW) return 2;
+    if (t.P == 1 && t.rows <= 4 * spt2::NG * spt2::NW) return 4;
+    return t.ns;
 }
 
 template <class Geo>

@@ -252,7 +252,7 @@ struct LinGeo2 {
     // Accumulators -> Out through LDS: ys[position][token], then each thread
     // writes one row position for a stride of tokens (row segments coalesce).
     template <int NSA>
-    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &, int64_t t0, int64_t row0,
+    __device__ void store(float *ys, const float (&acc)[NSA][4], const Tok &, int64_t t0, int64_t row0, int rp,
                           bool add) const {
         const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, g = lane >> 4, gl = lane & 15;
         __syncthreads();
@@ -263,12 +263,14 @@ struct LinGeo2 {
             for (int k = 0; k < 4; ++k) ys[pos * spt2::YS + 4 * gl + k] = acc[s][k];
         }
         __syncthreads();
-        constexpr int TSTEP = spt2::NTHR / spt2::R;
-        const int rl = tid % spt2::R;
+        // rp is 128 or 256: each thread owns row rl of the panel for every
+        // NTHR/rp-th token.
+        const int lg = rp == spt2::R ? 8 : 7;
+        const int rl = tid & (rp - 1);
         const int64_t row = row0 + rl;
         if (row < nrows) {
 #pragma unroll 4
-            for (int t = tid / spt2::R; t < spt2::T; t += TSTEP) {
+            for (int t = tid >> lg; t < spt2::T; t += spt2::NTHR >> lg) {
                 const int64_t gt = t0 + t;
                 if (gt < ntok) {
                     if (add)

@@ -11,7 +11,6 @@ using spt2::KC;
 using spt2::NG;
 using spt2::NS;
 using spt2::NW;
-using spt2::R;
 
 // cnt[r*K + k] = entries of row r in chunk k.  One wave per row.
 __global__ __launch_bounds__(256) void k_slot_count(const int32_t *__restrict__ ptr, const int32_t *__restrict__ idx,
@@ -22,17 +21,17 @@ __global__ __launch_bounds__(256) void k_slot_count(const int32_t *__restrict__ 
     for (int32_t j = ptr[r] + lane; j < ptr[r + 1]; j += 64) atomicAdd(&cnt[r * K + idx[j] / KC], 1);
 }
 
-// Row of position (w, g, s) in panel p, or -1.
-__device__ inline int64_t slot_row(int64_t p, int w, int g, int s, int64_t rows) {
-    const int64_t r = p * R + NG * NW * s + NG * w + g;
-    return r < rows ? r : -1;
+// Row of position (w, g, s) in panel p of a tiling with ns slots in use, or -1.
+__device__ inline int64_t slot_row(int64_t p, int w, int g, int s, int64_t rows, int ns) {
+    const int64_t r = p * (NG * NW * ns) + NG * NW * s + NG * w + g;
+    return s < ns && r < rows ? r : -1;
 }
 
 // One thread per (p, k, w): slot counts m_s = max over the groups of the run
 // lengths, packed into the header; the number of 16-iteration blocks goes to
 // nb[1 + (p*K + k)*NW + w] for the scan.
 __global__ __launch_bounds__(256) void k_slot_hdr(const int32_t *__restrict__ cnt, int64_t rows, int64_t P, int64_t K,
-                                                  int32_t *__restrict__ hdr, int32_t *__restrict__ nb) {
+                                                  int ns, int32_t *__restrict__ hdr, int32_t *__restrict__ nb) {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= P * K * NW) return;
     const int w = (int)(i % NW);
@@ -42,7 +41,7 @@ __global__ __launch_bounds__(256) void k_slot_hdr(const int32_t *__restrict__ cn
     for (int s = 0; s < NS; ++s) {
         int m = 0;
         for (int g = 0; g < NG; ++g) {
-            const int64_t r = slot_row(p, w, g, s, rows);
+            const int64_t r = slot_row(p, w, g, s, rows, ns);
             if (r >= 0) m = max(m, cnt[r * K + k]);
         }
         blocks += (m + 15) / 16;
@@ -69,12 +68,12 @@ __global__ void k_fill_meta(int2 *p, int64_t n, int2 v) {
 // chunk k goes to block base(p,k,w) + sum_{s'<s} ceil(m_s'/16) + j/16 at
 // position 4*(j%16) + g.
 __global__ __launch_bounds__(256) void k_slot_fill(const int32_t *__restrict__ ptr, const int32_t *__restrict__ idx,
-                                                   const int32_t *__restrict__ src_map, int64_t rows, int64_t K,
+                                                   const int32_t *__restrict__ src_map, int64_t rows, int64_t K, int rp,
                                                    const int32_t *__restrict__ hdr, int2 *__restrict__ meta) {
     const int64_t r = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (r >= rows) return;
-    const int64_t p = r / R;
-    const int pos = (int)(r % R);
+    const int64_t p = r / rp;
+    const int pos = (int)(r % rp);
     const int s = pos / (NG * NW), w = (pos % (NG * NW)) / NG, g = pos % NG;
     int64_t kprev = -1;
     int64_t blk = 0;
@@ -163,7 +162,7 @@ sp_status slot_build(const SlotTiling &t, const int32_t *ptr, const int32_t *idx
     }
     if (npkw > 0) {
         hipLaunchKernelGGL(k_slot_hdr, dim3((unsigned)sp::ceil_div(npkw, 256)), dim3(256), 0, st, cnt, t.rows, t.P,
-                           t.K, t.hdr, t.slotblk);
+                           t.K, t.ns, t.hdr, t.slotblk);
         SP_CHECK_LAUNCH();
     }
     if ((s = sp::scan_counts(t.slotblk, npkw, st))) return s;
@@ -174,7 +173,7 @@ sp_status slot_build(const SlotTiling &t, const int32_t *ptr, const int32_t *idx
     }
     if (t.rows > 0 && t.K > 0) {
         hipLaunchKernelGGL(k_slot_fill, dim3((unsigned)sp::ceil_div(t.rows, 256)), dim3(256), 0, st, ptr, idx,
-                           src_map, t.rows, t.K, t.hdr, t.meta);
+                           src_map, t.rows, t.K, NG * NW * t.ns, t.hdr, t.meta);
         SP_CHECK_LAUNCH();
     }
     return SP_OK;

@@ -37,7 +37,13 @@ constexpr int NW = 8;            // waves per workgroup
 constexpr int NTHR = NW * 64;
 constexpr int NG = 4;            // groups per wave
 constexpr int NS = 8;            // row slots per group
-constexpr int R = NW * NG * NS;  // rows per panel (256)
+constexpr int R = NW * NG * NS;  // rows of the tallest panel (256)
+// Convolution tilings of at most SHORT_ROWS rows use panels of R/2 rows (4
+// slots per group): twice the panels, so twice the workgroups for layers
+// whose token tiles are few, and no metadata for the upper slots.  A pure
+// function of the row count, so a plan serves every batch and image size.
+constexpr int SHORT_ROWS = 512;
+inline int panel_slots(int64_t rows) { return rows <= SHORT_ROWS ? NS / 2 : NS; }
 constexpr int KC = 256;          // columns per chunk
 constexpr int PF = KC * T / NTHR;  // staged floats per thread per chunk (32)
 constexpr int ZERO_OFF = KC * T * 4;  // byte offset of the zero column
@@ -51,25 +57,29 @@ struct SlotView {
     const int32_t *hdr;    // [P*K*NW*HDR]: first block of (p,k,w), then the slot counts m as 8 x u16
     const int2 *meta;      // [(nblocks + 3) * BLK] (LDS byte offset, value index or -1)
     int P, K;
+    int rp;                // rows per panel: 32 * slots in use
 };
 
 struct SlotTiling {
     int64_t rows, cols, P, K, nblk_cap;
+    int ns;           // slots in use per group (4 or 8): panels of 32*ns rows
     int32_t *hdr;     // P*K*NW*HDR
     int2 *meta;       // (nblk_cap + 3) * BLK: padding blocks past the last one absorb the prefetch
     int32_t *cnt;     // scratch rows*K (run counts), shared with other tilings
     int32_t *slotblk; // scratch P*K*NW*NS + 1 (block counts, scanned)
-    SlotView view() const { return SlotView{hdr, meta, (int)P, (int)K}; }
+    SlotView view() const { return SlotView{hdr, meta, (int)P, (int)K, NG * NW * ns}; }
 };
 
 // Upper bound of the number of metadata blocks: every (p,k,w,s) needs
 // ceil(max_g run / 16) <= (sum_g run)/16 + 1 blocks.
 inline int64_t slot_nblk_cap(int64_t nnz, int64_t P, int64_t K) { return nnz / 16 + P * K * NW * NS + 1; }
 
-inline void slot_layout(sp::Carve &c, SlotTiling &t, int64_t rows, int64_t cols, int64_t nnz) {
+// ns: slots in use per group, 4 or NS.
+inline void slot_layout(sp::Carve &c, SlotTiling &t, int64_t rows, int64_t cols, int64_t nnz, int ns = NS) {
     t.rows = rows;
     t.cols = cols;
-    t.P = sp::ceil_div(rows, R);
+    t.ns = ns;
+    t.P = sp::ceil_div(rows, (int64_t)NG * NW * t.ns);
     t.K = sp::ceil_div(cols, KC);
     t.nblk_cap = slot_nblk_cap(nnz, t.P, t.K);
     t.hdr = c.take<int32_t>(t.P * t.K * NW * HDR);
@@ -172,8 +182,9 @@ __device__ inline void slot_vals(float (&v)[PRE], const int2 (&m)[PRE], const fl
 //   uint32_t load_chunk(pf, tok, c0)      unconditional loads of one chunk into registers,
 //                                         returns a validity mask
 //   write_chunk(xs, pf, mask, tok)        registers -> xs[column][64 tokens] (zero where invalid)
-//   store(ys, acc, tok, t0, row0, add)   accumulators -> output (through LDS); with add,
-//                                         atomic adds into a zero-filled output
+//   store(ys, acc, tok, t0, row0, rp, add)  accumulators of the rp rows from row0 -> output
+//                                         (through LDS); with add, atomic adds into a
+//                                         zero-filled output
 // Work item L in [0, P*ntiles*nks) is one (panel, token tile) and a range of
 // the chunks: small problems split the chunks over nks = 2 workgroups, whose
 // two partial outputs meet in the zero-filled output by atomic adds -- exact
@@ -265,7 +276,7 @@ __device__ void spmm2_tile(const Geo &geo, const float *__restrict__ vals, const
             }
         }
     }
-    geo.store(xs, acc, tok, t0, (int64_t)p * R, nks > 1);
+    geo.store(xs, acc, tok, t0, (int64_t)p * tv.rp, tv.rp, nks > 1);
 }
 
 template <class Geo, int NSA = NS>
@@ -396,7 +407,7 @@ __device__ void sddmm2_tile(const Geo &geo, const SlotView &tv, int ntiles, int 
     const int q0 = j * tps, q1 = min(ntiles, q0 + tps);
     const int lp = 4 * (lane & 15) + (lane >> 4);
     const char *xb = reinterpret_cast<const char *>(xs) + (lane & 15) * 16;
-    const int64_t row0 = (int64_t)p * R;
+    const int64_t row0 = (int64_t)p * tv.rp;
 
     const int32_t *h = tv.hdr + (((int64_t)p * K + k) * NW + w) * HDR;
     const int b0 = h[0];
