@@ -491,6 +491,7 @@ struct ClassPart {
 
 struct ConvPlan {
     int32_t *t_ic_ptr, *t_oc, *t_perm;
+    int32_t *ptrA;          // [OC+1] entries of each output channel (a copy of w_oc)
     int32_t *colA, *colB;
     spt2::SlotTiling F, G;  // F: rows = OC, columns (ic, tap); G: rows = IC, columns (oc, tap)
     ClassPart cls[4];       // stride-2 input gradient, one per tap class
@@ -506,6 +507,7 @@ ConvPlan plan_layout(const void *base, const Dims &d, int64_t nnz) {
     L.t_ic_ptr = c.take<int32_t>(d.IC + 1);
     L.t_oc = c.take<int32_t>(nnz);
     L.t_perm = c.take<int32_t>(nnz);
+    L.ptrA = c.take<int32_t>(d.OC + 1);
     L.colA = c.take<int32_t>(nnz);
     L.colB = c.take<int32_t>(nnz);
     spt2::slot_layout(c, L.F, d.OC, d.IC * d.KK, nnz, spt2::panel_slots(d.OC));
@@ -713,6 +715,83 @@ sp_status spmm(const spt2::SlotTiling &t, const Geo &geo, const float *vals, int
 }
 
 // Full SpMM of one output tensor: zero-fill first when the chunks are split.
+// Direct forward for layers with at most FC_MAX input channels (image stems):
+// the im2col of such a layer has few columns, so the slot kernels' per-chunk
+// staging is spent on little work.  A workgroup computes a 16 x 16 block of
+// output pixels of one image for every output channel: the block's input
+// region (all channels, with its halo) is staged in LDS once, the stored
+// entries as (region offset, value), and each thread (one output pixel) walks
+// the entries of one output channel at a time -- wave-uniform LDS reads --
+// and writes that channel's pixel.
+constexpr int FC_MAX = 4;
+constexpr int FC_BLK = 16;             // output block edge
+constexpr int FC_XS = 8192;            // floats of input region staged (32 KB)
+constexpr int FC_ENT = 4096;           // entries staged (32 KB)
+
+__global__ __launch_bounds__(256) void k_fewcols_fwd(const float *__restrict__ X, float *__restrict__ Y,
+                                                      const int32_t *__restrict__ ptrA,
+                                                      const int32_t *__restrict__ colA,
+                                                      const float *__restrict__ vals, int nnz, int IC, int H, int W,
+                                                      int OC, int OH, int OW, int KW, int KK, int sh, int sw, int ph,
+                                                      int pw, int RH, int RW, int nbx, int nby) {
+    extern __shared__ float fc_lds[];
+    float *xs = fc_lds;                                                    // [IC][RH][RW]
+    int2 *ent = reinterpret_cast<int2 *>(fc_lds + ((IC * RH * RW + 1) & ~1));  // [nnz] (offset, value)
+    const int tid = threadIdx.x;
+    const int bx = (int)blockIdx.x % nbx, by = ((int)blockIdx.x / nbx) % nby, b = (int)blockIdx.x / (nbx * nby);
+    const int iy0 = by * FC_BLK * sh - ph, ix0 = bx * FC_BLK * sw - pw;
+    const int plane = RH * RW;
+    for (int i = tid; i < IC * plane; i += 256) {
+        const int ic = i / plane, q = i - ic * plane, ry = q / RW, rx = q - ry * RW;
+        const int iy = iy0 + ry, ix = ix0 + rx;
+        xs[i] = ((unsigned)iy < (unsigned)H && (unsigned)ix < (unsigned)W)
+                    ? X[(((int64_t)b * IC + ic) * H + iy) * W + ix]
+                    : 0.f;
+    }
+    for (int j = tid; j < nnz; j += 256) {
+        const int c = colA[j], ic = c / KK, tap = c - ic * KK, x = tap / KW, y = tap - x * KW;
+        ent[j] = make_int2(ic * plane + x * RW + y, __float_as_int(vals[j]));
+    }
+    __syncthreads();
+    const int ty = tid / FC_BLK, tx = tid % FC_BLK;
+    const int oy = by * FC_BLK + ty, ox = bx * FC_BLK + tx;
+    const bool ok = oy < OH && ox < OW;
+    const float *xp = xs + ty * sh * RW + tx * sw;
+    float *yp = Y + ((int64_t)b * OC * OH + oy) * OW + ox;
+    const int64_t ostride = (int64_t)OH * OW;
+    int j = ptrA[0];
+    for (int oc = 0; oc < OC; ++oc) {
+        const int j1 = ptrA[oc + 1];
+        float acc = 0.f;
+        for (; j < j1; ++j) {
+            const int2 e = ent[j - ptrA[0]];
+            acc = fmaf(__int_as_float(e.y), xp[e.x], acc);
+        }
+        if (ok) yp[oc * ostride] = acc;
+    }
+}
+
+// The direct forward applies when the block's input region and the entries
+// fit their LDS budgets.
+bool fewcols_fits(const Dims &d, int64_t nnz) {
+    const int64_t RH = (FC_BLK - 1) * (int64_t)d.sh + d.KH, RW = (FC_BLK - 1) * (int64_t)d.sw + d.KW;
+    return d.IC <= FC_MAX && d.IC * RH * RW <= FC_XS && nnz <= FC_ENT;
+}
+
+sp_status fewcols_fwd(const Dims &d, const ConvPlan &L, const float *X, const float *vals, int64_t nnz, float *Y,
+                      hipStream_t st) {
+    const int RH = (FC_BLK - 1) * d.sh + d.KH, RW = (FC_BLK - 1) * d.sw + d.KW;
+    const int nbx = (int)sp::ceil_div(d.OW, FC_BLK), nby = (int)sp::ceil_div(d.OH, FC_BLK);
+    const int64_t nwg = d.B * nbx * nby;
+    if (nwg > 0x7fffffffLL) return SP_ERR_UNSUPPORTED;
+    const size_t lds = (size_t)((d.IC * RH * RW + 1) & ~1) * 4 + (size_t)nnz * sizeof(int2);
+    hipLaunchKernelGGL(k_fewcols_fwd, dim3((unsigned)nwg), dim3(256), lds, st, X, Y, L.ptrA, L.colA, vals, (int)nnz,
+                       (int)d.IC, (int)d.H, (int)d.W, (int)d.OC, (int)d.OH, (int)d.OW, d.KW, d.KK, d.sh, d.sw, d.ph,
+                       d.pw, RH, RW, nbx, nby);
+    SP_CHECK_LAUNCH();
+    return SP_OK;
+}
+
 template <class Geo>
 sp_status spmm_full(const spt2::SlotTiling &t, const Geo &geo, const float *vals, float *out, int64_t out_elems,
                     hipStream_t st) {
@@ -1004,6 +1083,8 @@ extern "C" sp_status sp_conv_plan(const sp_conv_shape *s, const int32_t *w_oc, c
     if (plan_bytes < L.bytes) return SP_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     if ((r = transpose_build(d.OC, d.IC, w_oc, w_ic, nnz, L.t_ic_ptr, L.t_oc, L.t_perm, st))) return r;
+    if (hipMemcpyAsync(L.ptrA, w_oc, (d.OC + 1) * sizeof(int32_t), hipMemcpyDeviceToDevice, st) != hipSuccess)
+        return SP_ERR_HIP;
     if (nnz > 0) {
         hipLaunchKernelGGL(k_col_fwd, dim3((unsigned)sp::ceil_div(d.OC, 4)), dim3(256), 0, st, w_oc, w_ic, w_x, w_y,
                            d.OC, d.IC, d.KW, d.KK, L.colA);
@@ -1028,6 +1109,7 @@ extern "C" sp_status sp_conv_fwd(const float *X, const sp_conv_shape *s, const f
     hipStream_t st = (hipStream_t)stream;
     if (nnz == 0) return zero_launch(Y, d.B * d.OC * d.OH * d.OW, st);
     ConvPlan L = plan_layout(plan, d, nnz);
+    if (fewcols_fits(d, nnz)) return fewcols_fwd(d, L, X, w_vals, nnz, Y, st);
     ConvGeo<0> g = make_geo<0>(d, true);
     g.G = X;
     g.Out = Y;
