@@ -759,12 +759,14 @@ __global__ __launch_bounds__(256) void k_fewcols_fwd(const float *__restrict__ X
     const float *xp = xs + ty * sh * RW + tx * sw;
     float *yp = Y + ((int64_t)b * OC * OH + oy) * OW + ox;
     const int64_t ostride = (int64_t)OH * OW;
-    int j = ptrA[0];
+    // The format's first output channel starts at entry 0 (w_oc[0] = 0), so the
+    // table index is the entry index.
+    int j = 0;
     for (int oc = 0; oc < OC; ++oc) {
         const int j1 = ptrA[oc + 1];
         float acc = 0.f;
         for (; j < j1; ++j) {
-            const int2 e = ent[j - ptrA[0]];
+            const int2 e = ent[j];
             acc = fmaf(__int_as_float(e.y), xp[e.x], acc);
         }
         if (ok) yp[oc * ostride] = acc;
