@@ -83,29 +83,33 @@ COPY_BYTES = 1 << 30
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_spmm2_k_bwd_fused_ffn_pair_hbm_traffic.txt")
 FLUSH_BYTES = 1 << 30
 KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", "sp_linear.hip"]
+# The 3x3 64@56 convolution's counters (its backward dominates its step).
+CONV_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_conv_bwd_fused_conv3x3_56_hbm_traffic.txt")
+CONV_KERNEL_SOURCES = ["sp_common.h", "sp_common.hip", "sp_spmm2.h", "sp_slots.hip", "sp_conv.hip"]
 
 
-def kernel_source_hash():
-    """sha256 over the sources of the kernels the FFN bench launches."""
+def kernel_source_hash(sources=None):
+    """sha256 over the sources of the kernels a workload launches (default:
+    the FFN bench's)."""
     import hashlib
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in (KERNEL_SOURCES if sources is None else sources):
         with open(os.path.join(ROOT, "paper_2302_04852_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or
+def measured_traffic(kernel, path=None, sources=None):
+    """HBM bytes per launch of `kernel` from a committed counter summary, or
     None when it is absent or was taken on different kernel sources."""
     try:
-        lines = open(TRAFFIC_FILE).read().splitlines()
+        lines = open(TRAFFIC_FILE if path is None else path).read().splitlines()
     except OSError:
         return None
     for line in lines:
         if line.startswith("TRAFFIC "):
             rec = json.loads(line[len("TRAFFIC "):])
-            if rec.get("source_hash") == kernel_source_hash() and kernel in rec.get("bytes_per_launch", {}):
+            if rec.get("source_hash") == kernel_source_hash(sources) and kernel in rec.get("bytes_per_launch", {}):
                 return rec["bytes_per_launch"][kernel]
     return None
 
@@ -652,8 +656,12 @@ def run_conv(args, sp, torch, which):
     if kind.startswith("dense"):
         dl = [o[5] for o in ops if o[2] == kind and isinstance(o[5], ConvLayer)]
         mf = sum(L.dense_flops() * (2 if kind == "dense_bwd" else 1) for L in dl) / len(dl)
-    out["roofline"] = roofline(CONV_KERNEL[kind], kind, fl / n, by / n, t / n, None,
-                               {"launches_per_step": n, "note": "per-launch means over the workload's layers"}, mf)
+    traffic = None
+    if which == "conv3x3_56" and not kind.startswith("dense"):
+        traffic = measured_traffic(CONV_KERNEL[kind], CONV_TRAFFIC_FILE, CONV_KERNEL_SOURCES)
+    out["roofline"] = roofline(CONV_KERNEL[kind], kind, fl / n, by / n, t / n, traffic,
+                               {"launches_per_step": n, "note": "per-launch means over the workload's layers",
+                                "source_hash": kernel_source_hash(CONV_KERNEL_SOURCES)}, mf)
     out["by_op"] = {k: {"ms": round(v[0], 4), "tflops": round(v[1] / v[0] / 1e9, 3),
                         "alg_GBps": round(v[2] / v[0] / 1e6, 1), "bound": bound_of(v[1], v[2])}
                     for k, v in kinds.items()}
