@@ -165,10 +165,11 @@ def bound_of(flops, nbytes):
 # --------------------------------------------------------------------- layers
 
 def select_flags(sp, sparsity):
-    """The paper applies its 80% rule to a layer's pruning target; the synthetic
-    masks are Bernoulli draws that land a little above or below it.  Layers
-    pruned to 80% or more are therefore always timed; below that the
-    library's rule (dense, untimed) applies."""
+    """The paper applies its 80% rule to a layer's pruning target.  A mask
+    pruned to 80% holds round(0.2 * numel) entries, which the rounding can put
+    a fraction of an entry above 20% density, i.e. below 80% sparsity by the
+    library's count.  Layers pruned to 80% or more are therefore always timed;
+    below that the library's rule (dense, untimed) applies."""
     return sp.SP_SELECT_ALWAYS_TIME if sparsity >= 0.8 else 0
 
 
